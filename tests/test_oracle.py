@@ -1,0 +1,380 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Every check here reaches the oracle's result by another route: a library
+routine (torch's pre-LN encoder layer and multi-head attention, scipy's
+cosine distance), brute force on tiny inputs, or a closed form / invariant
+that the method's definition implies.  None of them runs the GPU library.
+"""
+import itertools
+import math
+
+import numpy as np
+import pytest
+import torch
+from scipy.spatial.distance import cosine as scipy_cosine
+
+from oracle import (MarOracle, attention, block_rows, cfg_reuse, cfg_store,
+                    cosine_scores, gelu, guided, layer_norm, select_least_similar,
+                    storage_round, value_rows)
+from paper_2503_12450_amd.workload import MarDims, all_block_weights, normal_rows, perturbed
+
+torch.backends.mha.set_fastpath_enabled(False)
+
+
+def _torch_layer(p, D, H, F, eps):
+    layer = torch.nn.TransformerEncoderLayer(
+        D, H, F, dropout=0.0, activation="gelu", layer_norm_eps=eps,
+        batch_first=True, norm_first=True, dtype=torch.float64)
+    t = lambda a: torch.from_numpy(np.asarray(a, dtype=np.float64))  # noqa: E731
+    with torch.no_grad():
+        layer.self_attn.in_proj_weight.copy_(t(p["qkv_w"]))
+        layer.self_attn.in_proj_bias.copy_(t(p["qkv_b"]))
+        layer.self_attn.out_proj.weight.copy_(t(p["proj_w"]))
+        layer.self_attn.out_proj.bias.copy_(t(p["proj_b"]))
+        layer.linear1.weight.copy_(t(p["fc1_w"]))
+        layer.linear1.bias.copy_(t(p["fc1_b"]))
+        layer.linear2.weight.copy_(t(p["fc2_w"]))
+        layer.linear2.bias.copy_(t(p["fc2_b"]))
+        layer.norm1.weight.copy_(t(p["ln1_w"]))
+        layer.norm1.bias.copy_(t(p["ln1_b"]))
+        layer.norm2.weight.copy_(t(p["ln2_w"]))
+        layer.norm2.bias.copy_(t(p["ln2_b"]))
+    layer.eval()
+    return layer
+
+
+def _torch_forward(layer, m):
+    with torch.no_grad():
+        return layer(torch.from_numpy(np.asarray(m, dtype=np.float64))[None])[0].numpy()
+
+
+TINY = MarDims(n_layers=4, d_model=32, n_heads=4, d_mlp=128, seq_len=12,
+               max_slots=4, full_prefix=2, dtype="f32")
+
+
+def _weights(dims, std=0.2):
+    # larger weights than the workload's so every term moves the result
+    from paper_2503_12450_amd.workload import block_weights
+    return [block_weights(dims, l, seed=7, std=std) for l in range(dims.n_layers)]
+
+
+# --------------------------------------------------------------------------
+# Building blocks
+# --------------------------------------------------------------------------
+
+def test_layer_norm_matches_torch_and_closed_form():
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((5, 24)) * 3 + 1
+    w, b = rng.standard_normal(24), rng.standard_normal(24)
+    ref = torch.nn.functional.layer_norm(torch.from_numpy(x), (24,), torch.from_numpy(w),
+                                         torch.from_numpy(b), eps=1e-6).numpy()
+    np.testing.assert_allclose(layer_norm(x, w, b, 1e-6), ref, rtol=0, atol=1e-13)
+    # a constant row normalises to the shift vector
+    np.testing.assert_allclose(layer_norm(np.full((1, 24), 3.5), w, b, 1e-6)[0], b, atol=1e-12)
+
+
+def test_gelu_exact_form():
+    x = np.linspace(-6, 6, 101)
+    ref = torch.nn.functional.gelu(torch.from_numpy(x)).numpy()
+    np.testing.assert_allclose(gelu(x), ref, rtol=0, atol=1e-15)
+    assert gelu(np.array([0.0]))[0] == 0.0
+    # Phi(1) = 0.841344746068543 (standard normal table)
+    assert abs(gelu(np.array([1.0]))[0] - 0.841344746068543) < 1e-14
+
+
+def _brute_attention(q, k, v):
+    out = []
+    dh = len(q[0])
+    for qi in q:
+        logits = [sum(qi[d] * kj[d] for d in range(dh)) / math.sqrt(dh) for kj in k]
+        m = max(logits)
+        w = [math.exp(l - m) for l in logits]
+        z = sum(w)
+        out.append([sum(w[j] * v[j][d] for j in range(len(k))) / z for d in range(len(v[0]))])
+    return np.array(out)
+
+
+@pytest.mark.parametrize("nq,nk,dh", [(1, 1, 1), (3, 7, 4), (4, 16, 8), (5, 5, 3)])
+def test_attention_brute_force(nq, nk, dh):
+    rng = np.random.default_rng(nq * 100 + nk)
+    q = rng.standard_normal((nq, dh)) * 2
+    k = rng.standard_normal((nk, dh)) * 2
+    v = rng.standard_normal((nk, dh))
+    np.testing.assert_allclose(attention(q, k, v), _brute_attention(q.tolist(), k.tolist(), v.tolist()),
+                               rtol=0, atol=1e-13)
+
+
+def test_attention_special_cases():
+    rng = np.random.default_rng(3)
+    k = rng.standard_normal((9, 4))
+    v = rng.standard_normal((9, 4))
+    # a zero query attends uniformly: the mean of the value rows
+    np.testing.assert_allclose(attention(np.zeros((1, 4)), k, v)[0], v.mean(axis=0), atol=1e-15)
+    # one key: the output is its value row
+    np.testing.assert_allclose(attention(rng.standard_normal((2, 4)), k[:1], v[:1]), np.repeat(v[:1], 2, 0),
+                               atol=1e-15)
+    # permuting keys and values together does not change anything
+    perm = rng.permutation(9)
+    q = rng.standard_normal((3, 4))
+    np.testing.assert_allclose(attention(q, k[perm], v[perm]), attention(q, k, v), atol=1e-14)
+
+
+def test_block_matches_torch_encoder_layer():
+    d = TINY
+    W = _weights(d)
+    m = normal_rows((d.seq_len, d.d_model), seed=5)
+    for l in range(2):
+        layer = _torch_layer(W[l], d.d_model, d.n_heads, d.d_mlp, d.ln_eps)
+        ref = _torch_forward(layer, m)
+        out, _ = block_rows(m, np.arange(d.seq_len), W[l], d.n_heads, d.ln_eps)
+        np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+
+
+def test_block_rows_subset_equals_full_rows():
+    # Eq. (9): a computed row sees every token's key/value, so its output is
+    # the full block's output for that row
+    d = TINY
+    W = _weights(d)
+    m = normal_rows((d.seq_len, d.d_model), seed=6)
+    layer = _torch_layer(W[1], d.d_model, d.n_heads, d.d_mlp, d.ln_eps)
+    ref = _torch_forward(layer, m)
+    rows = np.array([0, 3, 4, 11])
+    out, v = block_rows(m, rows, W[1], d.n_heads, d.ln_eps)
+    np.testing.assert_allclose(out, ref[rows], rtol=0, atol=1e-12)
+    # the value rows are torch's in-projection value slice
+    with torch.no_grad():
+        a = torch.nn.functional.layer_norm(torch.from_numpy(m.astype(np.float64)), (d.d_model,),
+                                           torch.from_numpy(W[1]["ln1_w"].astype(np.float64)),
+                                           torch.from_numpy(W[1]["ln1_b"].astype(np.float64)), eps=d.ln_eps)
+        _, _, vt = torch.nn.functional._in_projection_packed(
+            a, a, a, torch.from_numpy(W[1]["qkv_w"].astype(np.float64)),
+            torch.from_numpy(W[1]["qkv_b"].astype(np.float64)))
+    np.testing.assert_allclose(v, vt.numpy(), atol=1e-13)
+    np.testing.assert_allclose(value_rows(m, W[1], d.ln_eps), vt.numpy(), atol=1e-13)
+
+
+# --------------------------------------------------------------------------
+# Eq. (8): similarity and selection
+# --------------------------------------------------------------------------
+
+def test_cosine_matches_scipy_and_closed_forms():
+    rng = np.random.default_rng(11)
+    v = rng.standard_normal((20, 33))
+    r = v + 0.1 * rng.standard_normal((20, 33))
+    s = cosine_scores(v, r)
+    for i in range(20):
+        assert abs(s[i] - (1.0 - scipy_cosine(v[i], r[i]))) < 1e-14
+    # identical rows: exactly 1; opposite: -1; orthogonal: 0
+    assert np.all(cosine_scores(v, v) == 1.0)
+    np.testing.assert_allclose(cosine_scores(v, -v), -1.0, atol=1e-15)
+    e = np.eye(4)
+    assert np.all(cosine_scores(e, np.roll(e, 1, axis=0)) == 0.0)
+    # positive rescaling does not change the score
+    np.testing.assert_allclose(cosine_scores(v, 4.0 * r), s, atol=1e-15)
+    # zero rows (reading: 1 when both are zero, else 0)
+    z = np.zeros((2, 5))
+    o = np.ones((2, 5))
+    assert list(cosine_scores(z, z)) == [1.0, 1.0]
+    assert list(cosine_scores(z, o)) == [0.0, 0.0]
+    assert list(cosine_scores(o, z)) == [0.0, 0.0]
+
+
+def test_cosine_bf16_self_identity():
+    # scoring a stored row against itself gives exactly 1 in fp64
+    v = storage_round(np.random.default_rng(2).standard_normal((64, 1024)), "bf16")
+    assert np.all(cosine_scores(v, v.copy()) == 1.0)
+
+
+def _brute_select(s, n):
+    best = None
+    for c in itertools.combinations(range(len(s)), n):
+        key = (sum(s[i] for i in c), c)
+        if best is None or key < best:
+            best = key
+    return np.array(best[1] if best else (), dtype=np.int32)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_select_brute_force_with_ties(seed):
+    rng = np.random.default_rng(seed)
+    S = int(rng.integers(1, 10))
+    # multiples of 1/8 so the subset sums are exact and ties are real
+    s = rng.integers(-8, 9, size=S) / 8.0
+    for n in range(S + 1):
+        np.testing.assert_array_equal(select_least_similar(s, n), _brute_select(list(s), n))
+
+
+def test_select_special_cases():
+    s = np.array([0.3, 0.1, 0.9, 0.1, 0.5])
+    assert select_least_similar(s, 0).size == 0
+    np.testing.assert_array_equal(select_least_similar(s, 5), np.arange(5))
+    np.testing.assert_array_equal(select_least_similar(s, 2), [1, 3])
+    np.testing.assert_array_equal(select_least_similar(np.ones(7), 3), [0, 1, 2])
+    # NaN is treated as the most similar
+    np.testing.assert_array_equal(select_least_similar(np.array([np.nan, 0.5, 0.7]), 2), [1, 2])
+    # permuting tokens permutes the selection
+    rng = np.random.default_rng(1)
+    t = rng.standard_normal(40)
+    perm = rng.permutation(40)
+    a = set(select_least_similar(t, 13).tolist())
+    b = set(perm[select_least_similar(t[perm], 13)].tolist())
+    assert a == b
+    with pytest.raises(ValueError):
+        select_least_similar(s, 6)
+
+
+# --------------------------------------------------------------------------
+# Eq. (9): the cached step
+# --------------------------------------------------------------------------
+
+def _setup(dims, seed_prev=2):
+    W = _weights(dims)
+    o = MarOracle(dims, W)
+    x = normal_rows((2, dims.seq_len, dims.d_model), seed=1)
+    prev = perturbed(x, seed=seed_prev, std=0.3, dtype=dims.dtype)
+    return W, o, x, prev
+
+
+@pytest.mark.parametrize("P", [0, 1, 2])
+def test_full_recompute_ratio_equals_full_forward(P):
+    d = MarDims(3, 32, 4, 128, 12, 2, P, "f32")
+    W, o, x, prev = _setup(d)
+    o.full(prev)
+    y, idx, _ = o.cached(x, d.seq_len)
+    ref = MarOracle(d, W).full(x)
+    assert np.all(idx == np.arange(d.seq_len))
+    np.testing.assert_allclose(y, ref, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("P", [0, 2])
+@pytest.mark.parametrize("n", [0, 1, 5, 12])
+def test_unchanged_input_reuse_is_exact(P, n):
+    d = MarDims(3, 32, 4, 128, 12, 2, P, "f32")
+    W, o, x, _ = _setup(d)
+    y_full = o.full(x)
+    y, idx, s = o.cached(x, n)
+    assert np.all(s == 1.0)
+    np.testing.assert_array_equal(idx, np.tile(np.arange(n), (2, 1)))
+    np.testing.assert_allclose(y, y_full, rtol=0, atol=1e-12)
+
+
+def test_zero_recompute_returns_cache_and_updates_reference():
+    d = MarDims(3, 32, 4, 128, 12, 2, 1, "f32")
+    W, o, x, prev = _setup(d)
+    y_prev = o.full(prev)
+    y, idx, _ = o.cached(x, 0)
+    assert idx.shape == (2, 0)
+    np.testing.assert_array_equal(y, y_prev)
+    # the scoring reference now holds this step's value rows: the same input
+    # again scores 1 everywhere
+    _, _, s = o.cached(x, 0)
+    assert np.all(s == 1.0)
+
+
+def test_cached_rows_are_copies_and_selection_ignores_later_blocks():
+    d = MarDims(4, 32, 4, 128, 12, 2, 2, "f32")
+    W, o, x, prev = _setup(d)
+    y_prev = o.full(prev)
+    y, idx, s = o.cached(x, 5)
+    for b in range(2):
+        keep = np.setdiff1d(np.arange(d.seq_len), idx[b])
+        np.testing.assert_array_equal(y[b, keep], y_prev[b, keep])
+        assert not np.allclose(y[b, idx[b]], y_prev[b, idx[b]])
+    # changing blocks >= P changes neither the scores nor the selection
+    W2 = [dict(w) for w in W]
+    for l in range(d.full_prefix, d.n_layers):
+        W2[l] = {k: v * 1.5 for k, v in W2[l].items()}
+    o2 = MarOracle(d, W2)
+    o2.full(prev)
+    _, idx2, s2 = o2.cached(x, 5)
+    np.testing.assert_array_equal(idx2, idx)
+    np.testing.assert_array_equal(s2, s)
+
+
+@pytest.mark.parametrize("P", [0, 1, 2])
+def test_cached_step_equals_frozen_row_forward_through_torch(P):
+    """Eq. (9) by another route: run torch's encoder layers on the merged
+    state of every cached block (cached rows from the previous step, fresh
+    rows for the computed set) and keep the computed rows."""
+    d = MarDims(4, 32, 4, 128, 12, 2, P, "f32")
+    W, o, x, prev = _setup(d)
+    layers = [_torch_layer(w, d.d_model, d.n_heads, d.d_mlp, d.ln_eps) for w in W]
+    # previous step: full forward keeping every block's input/output
+    states = []
+    for b in range(2):
+        h = prev[b].astype(np.float64)
+        outs = [h]
+        for lay in layers:
+            h = _torch_forward(lay, h)
+            outs.append(h)
+        states.append(outs)   # outs[l] = input of block l
+    o.full(prev)
+    y, idx, _ = o.cached(x, 4)
+    for b in range(2):
+        h = x[b].astype(np.float64)
+        for l in range(P):
+            h = _torch_forward(layers[l], h)
+        fresh = h[idx[b]]
+        for l in range(P, d.n_layers):
+            merged = states[b][l].copy()
+            merged[idx[b]] = fresh
+            fresh = _torch_forward(layers[l], merged)[idx[b]]
+            states[b][l + 1][idx[b]] = fresh
+        np.testing.assert_allclose(y[b], states[b][d.n_layers], rtol=0, atol=1e-11)
+
+
+def test_given_rows_and_selection_agree():
+    d = MarDims(3, 32, 4, 128, 12, 2, 1, "f32")
+    W, o, x, prev = _setup(d)
+    o.full(prev)
+    y, idx, _ = o.cached(x, 6)
+    o2 = MarOracle(d, W)
+    o2.full(prev)
+    y2, idx2, _ = o2.cached(x, 6, given=idx)
+    np.testing.assert_array_equal(idx2, idx)
+    np.testing.assert_array_equal(y2, y)
+
+
+def test_cached_step_needs_a_fill():
+    d = MarDims(2, 32, 4, 128, 12, 2, 1, "f32")
+    o = MarOracle(d, _weights(d))
+    with pytest.raises(RuntimeError):
+        o.cached(normal_rows((1, 12, 32), seed=1), 3)
+
+
+# --------------------------------------------------------------------------
+# Eq. (7), (10): guidance and the condition cache
+# --------------------------------------------------------------------------
+
+def test_guidance_closed_forms():
+    rng = np.random.default_rng(4)
+    c = rng.standard_normal((3, 7))
+    u = rng.standard_normal((3, 7))
+    np.testing.assert_array_equal(guided(c, u, 0.0), u)
+    np.testing.assert_allclose(guided(c, u, 1.0), c, atol=1e-15)
+    np.testing.assert_allclose(guided(c, u, 0.5), (c + u) / 2, atol=1e-15)
+    np.testing.assert_allclose(guided(c, u, 4.0), u + 4.0 * (c - u), atol=1e-15)
+    stored, g = cfg_store(c, u, 2.5)
+    np.testing.assert_allclose(stored, u - c, atol=0)
+    # reusing on the same conditional output recovers the unconditional one
+    u_hat, g2 = cfg_reuse(c, stored, 2.5)
+    np.testing.assert_allclose(u_hat, u, atol=1e-15)
+    np.testing.assert_allclose(g2, g, atol=1e-14)
+    # with a new conditional output the residual carries over
+    c2 = c + 0.25
+    u_hat2, _ = cfg_reuse(c2, stored, 2.5)
+    np.testing.assert_allclose(u_hat2 - c2, u - c, atol=1e-15)
+
+
+def test_oracle_cfg_state():
+    d = MarDims(1, 32, 4, 128, 12, 4, 0, "f32")
+    o = MarOracle(d, _weights(d))
+    c = normal_rows((2, 12, 32), seed=3)
+    u = normal_rows((2, 12, 32), seed=4)
+    with pytest.raises(RuntimeError):
+        o.cfg("reuse", c, None, 3.0)
+    g, uu = o.cfg("store", c, u, 3.0)
+    np.testing.assert_array_equal(uu, u)
+    g2, uh = o.cfg("reuse", c, None, 3.0)
+    np.testing.assert_allclose(uh, u, atol=1e-6)
+    np.testing.assert_allclose(g2, g, atol=1e-5)
