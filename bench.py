@@ -1,0 +1,197 @@
+#!/usr/bin/env python3
+"""Throughput of LazyMAR's cached MAR transformer step on one MI355X.
+
+One bench step = one whole 64-decoding-step LazyMAR schedule for a batch of
+64 images x 2 guidance pathways at the MAR-L shape (16+16 blocks, width
+1024, 16 heads, 320 tokens, bf16): the steps before the 5th and the first
+step of every 9-step period are full steps (both pathways, every token);
+the other steps are token-cached with N = 50 recomputed rows per sequence,
+alternating conditional-only steps that reuse the stored guidance residual
+with two-pathway steps that store a fresh one; every step ends with the
+guidance combine.  Inputs of all 64 steps are resident in HBM before timing.
+
+Prints one JSON line.  --gpus N with N > 1 exits: this build runs on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3, help="timed schedules")
+    ap.add_argument("--warmup", type=int, default=1, help="untimed schedules")
+    ap.add_argument("--workload", default="mar-l", choices=["mar-l", "mar-b", "mar-h", "mar-l-hires"])
+    ap.add_argument("--profile-kind", default="fc1",
+                    help="kernel class timed with HIP events for the roofline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode-steps", type=int, default=64)
+    return ap.parse_args()
+
+
+def cpu_baseline(dims, W, recipe, n, plans):
+    """The oracle on the host cores: one full and one token-cached step of
+    one sequence, composed into one image's schedule."""
+    import numpy as np
+    import threadpoolctl
+
+    import oracle as O
+    from paper_2503_12450_amd import schedule as sch
+    from paper_2503_12450_amd.workload import step_input
+
+    threads = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()), default=1)
+    k = 20
+    prev = step_input(recipe, k - 1)[0]
+    x = step_input(recipe, k)[0]
+    orc = O.MarOracle(dims, W)
+    t0 = time.perf_counter()
+    orc.full_slot(0, prev)
+    t_full = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    orc.cached_slot(0, x, n)
+    t_cached = time.perf_counter() - t0
+    full, cond, both = sch.counts(plans)
+    seq_full = 2 * full
+    seq_cached = 2 * both + cond
+    t_sched = seq_full * t_full + seq_cached * t_cached
+    tokens = len(plans) * dims.seq_len
+    return {
+        "value": tokens / t_sched, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+        "sample": (f"fp64 numpy oracle, one sequence: one full step ({t_full:.2f} s) and one token-cached "
+                   f"step N={n} ({t_cached:.2f} s) at the {dims.n_layers}-block width-{dims.d_model} shape; "
+                   f"one image's schedule composed as {seq_full} full + {seq_cached} cached sequence-steps"),
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: the cached step shards over images with no "
+              "communication, and this build measures one GPU's share (see DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2503_12450_amd import binding as B
+    from paper_2503_12450_amd import flops as FL
+    from paper_2503_12450_amd import schedule as sch
+    from paper_2503_12450_amd.device import upload_blocks
+    from paper_2503_12450_amd.workload import WORKLOADS, all_block_weights, decode_recipe, step_inputs_device
+
+    wl = WORKLOADS[args.workload]
+    dims, n, images = wl.dims, wl.n_recompute, wl.images
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    W = all_block_weights(dims)
+    blocks = upload_blocks(W, dims.dtype, device=dev)
+    cache = B.MarCache(dims, blocks, device=dev)
+    torch.cuda.synchronize()
+    del blocks
+    recipe = decode_recipe(dims, images, args.decode_steps)
+    X = step_inputs_device(recipe, range(args.decode_steps), device=dev)
+    cfg_rule = "paper" if args.workload == "mar-l-hires" else "alternate"
+    plans = sch.lazymar_schedule(args.decode_steps, 5, 9, cfg_rule)
+    Y = cache.output()
+    guided = torch.empty((images, dims.seq_len, dims.d_model), dtype=torch.float32, device=dev)
+    scale = 4.0
+
+    def one_step(p, x, ev=None):
+        if p.mode == sch.FULL:
+            cache.step(x, B.MAR_FULL)
+        elif p.branches == sch.BOTH:
+            cache.step(x, B.MAR_TOKEN_CACHED, n)
+        else:
+            cache.step(x[:images], B.MAR_TOKEN_CACHED, n, slot0=0)
+        if p.cfg == sch.STORE:
+            cache.cfg_combine(B.MAR_CFG_STORE, Y[:images], Y[images:2 * images], scale, guided)
+        else:
+            cache.cfg_combine(B.MAR_CFG_REUSE, Y[:images], None, scale, guided)
+
+    def schedule_run(step_events=None):
+        for i, p in enumerate(plans):
+            if step_events is not None:
+                step_events[i][0].record()
+            one_step(p, X[i])
+            if step_events is not None:
+                step_events[i][1].record()
+
+    for _ in range(args.warmup):
+        schedule_run()
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` schedules
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in plans] for _ in range(args.steps)]
+    cache.profile_start(args.profile_kind)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        schedule_run(evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    prof_ms, prof_n, prof_flops, prof_bytes = cache.profile_stop()
+
+    per_mode = {"full": [], "cached_both": [], "cached_cond": []}
+    for k in range(args.steps):
+        for p, (a, b) in zip(plans, evs[k]):
+            key = "full" if p.mode == sch.FULL else ("cached_both" if p.branches == sch.BOTH else "cached_cond")
+            per_mode[key].append(a.elapsed_time(b))
+    mean = {k: (float(np.mean(v)) if v else None) for k, v in per_mode.items()}
+
+    ms_per_sched = 1e3 * wall / args.steps
+    tokens_per_sched = len(plans) * images * dims.seq_len
+    value = tokens_per_sched / (ms_per_sched / 1e3)
+    sched_flops = 0
+    for p in plans:
+        if p.mode == sch.FULL:
+            sched_flops += FL.step_flops(dims, 2 * images, "full")
+        else:
+            sched_flops += FL.step_flops(dims, (2 if p.branches == sch.BOTH else 1) * images, "cached", n)
+    full_sched_ms = len(plans) * mean["full"]
+
+    achieved = prof_flops / (prof_ms / 1e3) / 1e12 if prof_ms > 0 else None
+    roofline = {
+        "kernel": f"{args.profile_kind} product (bf16 MFMA, fp32 accumulate)",
+        "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+        "frac": (achieved / PEAK_BF16_TFLOPS) if achieved else None,
+        "traffic": None,
+        "launches": prof_n, "avg_launch_us": 1e3 * prof_ms / max(prof_n, 1),
+        "flops_per_launch": prof_flops / max(prof_n, 1),
+        "bytes_per_launch": prof_bytes / max(prof_n, 1),
+    }
+    line = {
+        "metric": "cached MAR step tokens/s (MAR-L, 64x2 CFG, 64-step LazyMAR schedule)",
+        "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_per_sched, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": dims.dtype, "data": "synthetic",
+        "config": {"workload": wl.name, "images": images, "seq_len": dims.seq_len,
+                   "n_recompute": n, "decode_steps": len(plans),
+                   "schedule": "start 5, tau 9, " + cfg_rule + " guidance reuse",
+                   "step": "one 64-decoding-step schedule"},
+        "tflops": sched_flops / (ms_per_sched / 1e3) / 1e12,
+        "step_ms": mean,
+        "speedup_vs_full_recompute": full_sched_ms / ms_per_sched if mean["full"] else None,
+        "speedup_cached_cond_vs_full": (mean["full"] / mean["cached_cond"]) if mean["cached_cond"] else None,
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(dims, W, recipe, n, plans)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -22,7 +22,8 @@ Readings of the paper taken here (the paper is silent or garbled on them):
   With no always-computed block, the value rows of block 0 are formed from
   the step's input for scoring only.
 * The value rows are scored as the path stores them (bfloat16 or float32);
-  products and sums are fp64.  Zero norms: 1 when both rows are zero, else
+  the products are exact in fp64 and each dot product is their exactly
+  rounded fp64 sum, so the score does not depend on a summation order.  Zero norms: 1 when both rows are zero, else
   0.  A NaN score ranks as +inf (most similar).
 * Ties go to the lower token index; selected indices are returned ascending.
 * Rows that are not computed keep the cached state of the previous block's
@@ -141,16 +142,29 @@ def storage_round(a, dtype: str) -> np.ndarray:
     raise ValueError(f"unknown dtype {dtype!r}")
 
 
+def _exact_dot(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """Row dot products summed exactly and rounded once to fp64.
+
+    The products of stored fp32/bf16 values are exact in fp64; math.fsum
+    returns their exactly rounded sum, so the value does not depend on any
+    summation order.
+    """
+    p = (a * b).reshape(-1, a.shape[-1])
+    out = np.fromiter((math.fsum(row) for row in p.tolist()), dtype=np.float64, count=p.shape[0])
+    return out.reshape(a.shape[:-1])
+
+
 def cosine_scores(v, r) -> np.ndarray:
     """Eq. (8): S(x_i) = <v_i, r_i> / (||v_i|| ||r_i||) for every row i.
 
     v are this step's value rows, r the cached ones of the previous step.
-    Products and sums in fp64.  Zero norms: 1 if both rows are zero, else 0.
+    The three dot products are exactly rounded fp64 values; then
+    s = dot / sqrt(|v|^2 |r|^2).  Zero norms: 1 if both rows are zero, else 0.
     """
     v, r = _f64(v), _f64(r)
-    dot = np.einsum("...d,...d->...", v, r)
-    nv = np.einsum("...d,...d->...", v, v)
-    nr = np.einsum("...d,...d->...", r, r)
+    dot = _exact_dot(v, r)
+    nv = _exact_dot(v, v)
+    nr = _exact_dot(r, r)
     den = np.sqrt(nv * nr)
     with np.errstate(invalid="ignore", divide="ignore"):
         s = dot / den

@@ -1,0 +1,142 @@
+// Shared device helpers and launcher declarations of the cached MAR step.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace marcache {
+
+typedef uint16_t bf16_t;  // bfloat16 bits
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4_t;
+typedef __attribute__((ext_vector_type(16))) float f32x16_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2_t;
+
+enum Dtype { DT_F32 = 0, DT_BF16 = 1 };
+
+__device__ __forceinline__ float bf2f(bf16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// fp32 -> bf16, round to nearest even (the hardware conversion on gfx950).
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  __bf16 b = static_cast<__bf16>(f);
+  return __builtin_bit_cast(bf16_t, b);
+}
+
+// Element traits: storage type <-> fp32.
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  static __device__ __forceinline__ float load(const float* p) { return *p; }
+  static __device__ __forceinline__ float to_f(float v) { return v; }
+  static __device__ __forceinline__ float from_f(float v) { return v; }
+  static constexpr int kPer16B = 4;
+};
+template <> struct Elem<bf16_t> {
+  static __device__ __forceinline__ float to_f(bf16_t v) { return bf2f(v); }
+  static __device__ __forceinline__ bf16_t from_f(float v) { return f2bf(v); }
+  static constexpr int kPer16B = 8;
+};
+
+// Unpack one 16-byte vector of storage elements to fp32.
+__device__ __forceinline__ void unpack16(const u32x4_t& v, float* out, const float*) {
+  out[0] = __uint_as_float(v[0]);
+  out[1] = __uint_as_float(v[1]);
+  out[2] = __uint_as_float(v[2]);
+  out[3] = __uint_as_float(v[3]);
+}
+__device__ __forceinline__ void unpack16(const u32x4_t& v, float* out, const bf16_t*) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    out[2 * i] = __uint_as_float(v[i] << 16);
+    out[2 * i + 1] = __uint_as_float(v[i] & 0xFFFF0000u);
+  }
+}
+
+__device__ __forceinline__ uint32_t pack2bf(float lo, float hi) {
+  return static_cast<uint32_t>(f2bf(lo)) | (static_cast<uint32_t>(f2bf(hi)) << 16);
+}
+
+// Butterfly sums across the 64 lanes of a wave; every lane gets the total.
+// The order of additions is fixed, so the result is deterministic.
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// Launchers (host side).  All return hipSuccess or the launch error.
+// Rows of a "slot-mapped" matrix: row m belongs to slot m / per_slot and to
+// token idx[m] (or m % per_slot when idx is null) of that slot.
+// ---------------------------------------------------------------------------
+
+// Row LayerNorm: out[m] = LN(src_row(m)) in dtype, optional fp32 copy of the
+// source row.  src_row(m) = src[(m / per_slot) * seq + tok(m)] where tok(m)
+// = idx[m] when idx is given, else m % per_slot (then seq must equal
+// per_slot).  src is fp32 when src_f32, else the storage dtype.
+hipError_t launch_layernorm(int dtype, const void* src, bool src_f32, const int32_t* idx,
+                            int per_slot, int seq, int M, int D, const float* w,
+                            const float* b, float eps, float* copy_f32, void* out,
+                            hipStream_t st);
+
+// Epilogue kinds of the matrix product C = A W^T (A [M,K], W [N,K]).
+enum EpiKind {
+  EPI_BIAS = 0,      // out[m, n] = C + bias[n]                        (dtype)
+  EPI_GELU = 1,      // out[m, n] = gelu(C + bias[n])                  (dtype)
+  EPI_RESIDUAL = 2,  // out[row(m), n] = resid[m, n] + C + bias[n]     (fp32)
+  EPI_QKV = 3        // split into q rows and key/value cache rows     (dtype)
+};
+
+struct EpiArgs {
+  int kind;
+  const float* bias;
+  void* out;           // BIAS/GELU: [M, N]; RESIDUAL: fp32 rows; QKV: q [M, D]
+  const float* resid;  // RESIDUAL: fp32 [M, N] (may equal out when no remap)
+  // RESIDUAL remap: when out_idx is non-null, row m goes to
+  //   out[(m / per_slot) * seq + out_idx[m]] (the output-cache scatter);
+  //   resid_copy (nullable) also receives the row at m.
+  const int32_t* out_idx;
+  float* resid_copy;
+  // QKV: n_global = n + n_offset selects q (< D), k (< 2D) or v; key/value
+  // rows go to cache[(slot * H + head) * seq + tok][d] with slot/tok from the
+  // row mapping (idx or dense).
+  int n_offset;
+  int d_model, n_heads, d_head, seq, per_slot;
+  const int32_t* idx;
+  void* k_cache;
+  void* v_cache;
+  void* v_copy;  // nullable second destination of value rows (same layout)
+};
+
+hipError_t launch_gemm(int dtype, const void* A, const void* W, int M, int N, int K,
+                       const EpiArgs& epi, hipStream_t st);
+
+// Attention of per_slot queries per slot against the seq keys of the slot:
+// q, out [n_slots * per_slot, D] (head h at columns h*dh..); k, v
+// [n_slots, H, seq, dh].
+hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v, void* out,
+                            int n_slots, int H, int seq, int dh, int per_slot,
+                            hipStream_t st);
+
+// Cosine scores of value rows (Eq. 8) for [n_slots, H, seq, dh] layouts;
+// optionally copies v_cur into v_ref afterwards.
+hipError_t launch_scores(int dtype, const void* v_cur, void* v_ref, int n_slots, int H,
+                         int seq, int dh, double* scores, bool update_ref, hipStream_t st);
+
+// The n least similar tokens of each slot, ascending.
+hipError_t launch_select(const double* scores, int n_slots, int seq, int n, int32_t* idx,
+                         hipStream_t st);
+
+// Guidance with the condition cache over `count` fp32 elements.
+hipError_t launch_cfg(int op, const float* c, const float* u, float* stored, float scale,
+                      float* guided, float* u_out, size_t count, hipStream_t st);
+
+}  // namespace marcache

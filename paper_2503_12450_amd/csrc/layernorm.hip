@@ -1,0 +1,131 @@
+// Row LayerNorm of the pre-LN block, optionally gathering the rows first.
+//
+// One wave per row.  Each lane holds groups of 8 consecutive elements in
+// registers (16-byte bf16 or 2x16-byte fp32 loads), so the statistics are a
+// two-pass mean / biased variance over values already in registers, summed
+// with a fixed butterfly order (the result of a row never depends on which
+// other rows are in the launch).  As the gather for the cached blocks
+// (Eq. 9: only the computed rows enter blocks P..L-1), row m reads token
+// idx[m] of its slot and the fp32 copy of that row seeds the compact
+// residual stream.
+#include "common.h"
+
+namespace marcache {
+
+constexpr int kLnMaxGroups = 4;  // 4 groups x 8 elements x 64 lanes: D <= 2048
+
+template <typename TIn>
+__device__ __forceinline__ void load8(const TIn* p, float* v);
+template <>
+__device__ __forceinline__ void load8<float>(const float* p, float* v) {
+  const u32x4_t a = *reinterpret_cast<const u32x4_t*>(p);
+  const u32x4_t b = *reinterpret_cast<const u32x4_t*>(p + 4);
+  unpack16(a, v, static_cast<const float*>(nullptr));
+  unpack16(b, v + 4, static_cast<const float*>(nullptr));
+}
+template <>
+__device__ __forceinline__ void load8<bf16_t>(const bf16_t* p, float* v) {
+  const u32x4_t a = *reinterpret_cast<const u32x4_t*>(p);
+  unpack16(a, v, static_cast<const bf16_t*>(nullptr));
+}
+
+template <typename TOut>
+__device__ __forceinline__ void store8(TOut* p, const float* v);
+template <>
+__device__ __forceinline__ void store8<float>(float* p, const float* v) {
+  u32x4_t a, b;
+  for (int i = 0; i < 4; ++i) {
+    a[i] = __float_as_uint(v[i]);
+    b[i] = __float_as_uint(v[4 + i]);
+  }
+  *reinterpret_cast<u32x4_t*>(p) = a;
+  *reinterpret_cast<u32x4_t*>(p + 4) = b;
+}
+template <>
+__device__ __forceinline__ void store8<bf16_t>(bf16_t* p, const float* v) {
+  u32x4_t a;
+  for (int i = 0; i < 4; ++i) a[i] = pack2bf(v[2 * i], v[2 * i + 1]);
+  *reinterpret_cast<u32x4_t*>(p) = a;
+}
+
+template <typename TIn, typename TOut>
+__global__ __launch_bounds__(256) void layernorm_kernel(const TIn* __restrict__ src,
+                                                        const int32_t* __restrict__ idx,
+                                                        int per_slot, int seq, int M, int D,
+                                                        const float* __restrict__ w,
+                                                        const float* __restrict__ bias,
+                                                        float eps, float* __restrict__ copy_f32,
+                                                        TOut* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const long m = static_cast<long>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (m >= M) return;
+  const long slot = m / per_slot;
+  const long tok = idx ? static_cast<long>(idx[m]) : (m - slot * per_slot);
+  const TIn* row = src + (slot * seq + tok) * D;
+  const int groups = D / 8;
+  float v[kLnMaxGroups][8];
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < kLnMaxGroups; ++i) {
+    const int g = lane + 64 * i;
+    if (g < groups) {
+      load8<TIn>(row + g * 8, v[i]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) sum += v[i][j];
+    }
+  }
+  const float mean = wave_sum(sum) / static_cast<float>(D);
+  float sq = 0.f;
+#pragma unroll
+  for (int i = 0; i < kLnMaxGroups; ++i) {
+    const int g = lane + 64 * i;
+    if (g < groups) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float d = v[i][j] - mean;
+        sq += d * d;
+      }
+    }
+  }
+  const float var = wave_sum(sq) / static_cast<float>(D);
+  const float rstd = 1.0f / sqrtf(var + eps);
+#pragma unroll
+  for (int i = 0; i < kLnMaxGroups; ++i) {
+    const int g = lane + 64 * i;
+    if (g < groups) {
+      if (copy_f32) store8<float>(copy_f32 + m * D + g * 8, v[i]);
+      float o[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int e = g * 8 + j;
+        o[j] = (v[i][j] - mean) * rstd * w[e] + bias[e];
+      }
+      store8<TOut>(out + m * D + g * 8, o);
+    }
+  }
+}
+
+template <typename TIn, typename TOut>
+static hipError_t ln_launch(const void* src, const int32_t* idx, int per_slot, int seq, int M,
+                            int D, const float* w, const float* b, float eps, float* copy_f32,
+                            void* out, hipStream_t st) {
+  dim3 grid(static_cast<unsigned>((M + 3) / 4));
+  hipLaunchKernelGGL((layernorm_kernel<TIn, TOut>), grid, dim3(256), 0, st,
+                     static_cast<const TIn*>(src), idx, per_slot, seq, M, D, w, b, eps,
+                     copy_f32, static_cast<TOut*>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_layernorm(int dtype, const void* src, bool src_f32, const int32_t* idx,
+                            int per_slot, int seq, int M, int D, const float* w, const float* b,
+                            float eps, float* copy_f32, void* out, hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  if (dtype == DT_BF16) {
+    if (src_f32)
+      return ln_launch<float, bf16_t>(src, idx, per_slot, seq, M, D, w, b, eps, copy_f32, out, st);
+    return ln_launch<bf16_t, bf16_t>(src, idx, per_slot, seq, M, D, w, b, eps, copy_f32, out, st);
+  }
+  return ln_launch<float, float>(src, idx, per_slot, seq, M, D, w, b, eps, copy_f32, out, st);
+}
+
+}  // namespace marcache

@@ -294,3 +294,37 @@ def step_input(recipe: DecodeRecipe, step: int) -> np.ndarray:
     x += recipe.pos[None]
     del T
     return to_storage(x, recipe.dims.dtype)
+
+
+def step_inputs_device(recipe: DecodeRecipe, steps, device="cuda"):
+    """step_input() for several steps, assembled on the device with torch
+    (same recipe; fp32 arithmetic, then the storage dtype).  Returns a list
+    of [2B, S, D] tensors."""
+    import torch
+
+    dims = recipe.dims
+    B, S, D = recipe.images, dims.seq_len, dims.d_model
+    T = recipe.image_tokens
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16}[dims.dtype]
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)  # noqa: E731
+    zp = dev(recipe.z) @ dev(recipe.proj)                 # [B, T, D]
+    mask_vec = dev(recipe.mask_vec)
+    pos = dev(recipe.pos)
+    cls = dev(recipe.cls)
+    rank = torch.empty((B, T), dtype=torch.int64, device=device)
+    order = dev(recipe.order)
+    rank.scatter_(1, order, torch.arange(T, device=device).expand(B, T).contiguous())
+    out = []
+    for k in steps:
+        n_dec = T - int(recipe.counts[k])
+        dec = (rank < n_dec)[:, :, None]
+        img = torch.where(dec, zp, mask_vec[None, None, :])
+        x = torch.empty((2 * B, S, D), dtype=torch.float32, device=device)
+        x[:B, :BUFFER_ROWS] = cls[:, None, :]
+        x[B:, :BUFFER_ROWS] = 0.0
+        x[:B, BUFFER_ROWS:] = img
+        x[B:, BUFFER_ROWS:] = img
+        x += pos[None]
+        out.append(x.to(tdt).contiguous())
+        del x, img, dec
+    return out

@@ -1,0 +1,263 @@
+"""Per-kernel parity of the HIP library against the CPU oracle.
+
+Both sides take the same seeded inputs; the GPU result is compared element
+by element with the oracle's fp64 result.  Tolerances: fp32 storage max-abs
+1e-4 (plus 1e-5 relative); bf16 storage max-abs 2e-2 with 1e-2 relative,
+the bar for bf16 activations.  Integer work (selection, gathers, scatters)
+is compared bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2503_12450_amd import binding as B
+from paper_2503_12450_amd.device import to_device
+from paper_2503_12450_amd.workload import normal_rows, random_index_sets, to_storage
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": dict(atol=1e-4, rtol=1e-5), "bf16": dict(atol=2e-2, rtol=1e-2)}
+DEV = "cuda"
+
+
+def _host(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def _close(got, want, dtype, what=""):
+    np.testing.assert_allclose(_host(got) if torch.is_tensor(got) else got, want, err_msg=what, **TOL[dtype])
+
+
+def _cache_layout(rows, H):
+    """[slots, S, D] rows -> [slots, H, S, dh]"""
+    s, S, D = rows.shape
+    return np.ascontiguousarray(rows.reshape(s, S, H, D // H).transpose(0, 2, 1, 3))
+
+
+# --------------------------------------------------------------------------
+# LayerNorm (with and without the row gather)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("M,D", [(1, 64), (300, 256), (77, 1280), (5, 2048)])
+def test_layernorm_dense(dtype, M, D):
+    src = normal_rows((M, D), seed=11, std=2.0) + 0.5
+    w = 1.0 + normal_rows((D,), seed=12, std=0.2)
+    b = normal_rows((D,), seed=13, std=0.2)
+    out = torch.empty((M, D), dtype=to_device(src[:1], dtype).dtype, device=DEV)
+    B.k_layernorm(dtype, to_device(src, "f32"), to_device(w, "f32"), to_device(b, "f32"), 1e-6, out)
+    torch.cuda.synchronize()
+    _close(out, O.layer_norm(src, w, b, 1e-6), dtype)
+
+
+@pytest.mark.parametrize("dtype,src_dtype", [("f32", "f32"), ("bf16", "f32"), ("bf16", "bf16")])
+def test_layernorm_gather(dtype, src_dtype):
+    slots, S, D, N = 3, 50, 256, 7
+    src = normal_rows((slots, S, D), seed=14, dtype=src_dtype)
+    idx = random_index_sets(slots, S, N, seed=15)
+    w = 1.0 + normal_rows((D,), seed=16, std=0.2)
+    b = normal_rows((D,), seed=17, std=0.2)
+    out = torch.empty((slots * N, D), dtype=to_device(src[:1, :1], dtype).dtype, device=DEV)
+    copy = torch.full((slots * N, D), 7.0, dtype=torch.float32, device=DEV)
+    B.k_layernorm(dtype, to_device(src, src_dtype), to_device(w, "f32"), to_device(b, "f32"), 1e-6, out,
+                  idx=torch.from_numpy(idx).to(DEV), per_slot=N, seq=S, copy_f32=copy)
+    torch.cuda.synchronize()
+    gathered = np.concatenate([src[s, idx[s]] for s in range(slots)])
+    np.testing.assert_array_equal(copy.cpu().numpy(), gathered)   # the gather is exact
+    _close(out, O.layer_norm(gathered, w, b, 1e-6), dtype)
+
+
+# --------------------------------------------------------------------------
+# Matrix products with their epilogues
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (300, 320, 256), (129, 1024, 1024), (1000, 192, 3072)])
+@pytest.mark.parametrize("gelu", [False, True])
+def test_linear(dtype, M, N, K, gelu):
+    a = normal_rows((M, K), seed=21, dtype=dtype)
+    w = normal_rows((N, K), seed=22, std=0.05, dtype=dtype)
+    bias = normal_rows((N,), seed=23, std=0.5)
+    out = torch.empty((M, N), dtype=to_device(a[:1], dtype).dtype, device=DEV)
+    B.k_linear(dtype, to_device(a, dtype), to_device(w, dtype), to_device(bias, "f32"), out, gelu=gelu)
+    torch.cuda.synchronize()
+    ref = O.linear(a, w, bias)
+    if gelu:
+        ref = O.gelu(ref)
+    _close(out, ref, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_linear_residual_in_place_and_scatter(dtype):
+    M, N, K = 200, 256, 512
+    a = normal_rows((M, K), seed=31, dtype=dtype)
+    w = normal_rows((N, K), seed=32, std=0.05, dtype=dtype)
+    bias = normal_rows((N,), seed=33, std=0.5)
+    resid = normal_rows((M, N), seed=34)
+    r = to_device(resid, "f32")
+    B.k_linear_residual(dtype, to_device(a, dtype), to_device(w, dtype), to_device(bias, "f32"), r, r)
+    torch.cuda.synchronize()
+    ref = resid + O.linear(a, w, bias)
+    _close(r, ref, dtype)
+    # scatter into an output cache [slots, S, N] at per-slot token indices
+    slots, S = 4, 120
+    per = M // slots
+    idx = random_index_sets(slots, S, per, seed=35)
+    ycache = torch.full((slots, S, N), -3.0, dtype=torch.float32, device=DEV)
+    copy = torch.zeros((M, N), dtype=torch.float32, device=DEV)
+    r2 = to_device(resid, "f32")
+    B.k_linear_residual(dtype, to_device(a, dtype), to_device(w, dtype), to_device(bias, "f32"), r2, ycache,
+                        out_idx=torch.from_numpy(idx.reshape(-1)).to(DEV), per_slot=per, seq=S, resid_copy=copy)
+    torch.cuda.synchronize()
+    yc = ycache.cpu().numpy()
+    for s in range(slots):
+        _close(yc[s, idx[s]], ref[s * per:(s + 1) * per], dtype)
+        untouched = np.setdiff1d(np.arange(S), idx[s])
+        assert np.all(yc[s, untouched] == -3.0)
+    _close(copy, ref, dtype)
+    np.testing.assert_array_equal(r2.cpu().numpy(), resid)  # resid is read only here
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("D,H", [(128, 2), (320, 4), (256, 16)])
+def test_qkv_dense_and_scattered(dtype, D, H):
+    slots, S = 3, 70
+    dh = D // H
+    M = slots * S
+    a = normal_rows((M, D), seed=41, dtype=dtype)
+    w = normal_rows((3 * D, D), seed=42, std=0.05, dtype=dtype)
+    bias = normal_rows((3 * D,), seed=43, std=0.5)
+    ref = O.linear(a, w, bias)
+    td = to_device(a[:1], dtype).dtype
+    q = torch.empty((M, D), dtype=td, device=DEV)
+    kc = torch.zeros((slots, H, S, dh), dtype=td, device=DEV)
+    vc = torch.zeros((slots, H, S, dh), dtype=td, device=DEV)
+    vcopy = torch.zeros((slots, H, S, dh), dtype=td, device=DEV)
+    B.k_qkv(dtype, to_device(a, dtype), to_device(w, dtype), to_device(bias, "f32"), D, H, S, S,
+            q_out=q, k_cache=kc, v_cache=vc, v_copy=vcopy)
+    torch.cuda.synchronize()
+    _close(q, ref[:, :D], dtype)
+    _close(kc, _cache_layout(ref[:, D:2 * D].reshape(slots, S, D), H), dtype)
+    _close(vc, _cache_layout(ref[:, 2 * D:].reshape(slots, S, D), H), dtype)
+    np.testing.assert_array_equal(_host(vcopy), _host(vc))
+    # compact rows: keys/values land at their tokens, other rows untouched
+    N = 9
+    idx = random_index_sets(slots, S, N, seed=44)
+    ac = normal_rows((slots * N, D), seed=45, dtype=dtype)
+    refc = O.linear(ac, w, bias)
+    kc2 = torch.full((slots, H, S, dh), 5.0, dtype=td, device=DEV)
+    vc2 = torch.full((slots, H, S, dh), 5.0, dtype=td, device=DEV)
+    qc = torch.empty((slots * N, D), dtype=td, device=DEV)
+    B.k_qkv(dtype, to_device(ac, dtype), to_device(w, dtype), to_device(bias, "f32"), D, H, S, N,
+            q_out=qc, k_cache=kc2, v_cache=vc2, idx=torch.from_numpy(idx.reshape(-1)).to(DEV))
+    torch.cuda.synchronize()
+    _close(qc, refc[:, :D], dtype)
+    k2, v2 = _host(kc2), _host(vc2)
+    for s in range(slots):
+        rows = refc[s * N:(s + 1) * N]
+        _close(k2[s][:, idx[s]], rows[:, D:2 * D].reshape(N, H, dh).transpose(1, 0, 2), dtype)
+        _close(v2[s][:, idx[s]], rows[:, 2 * D:].reshape(N, H, dh).transpose(1, 0, 2), dtype)
+        other = np.setdiff1d(np.arange(S), idx[s])
+        assert np.all(k2[s][:, other] == 5.0) and np.all(v2[s][:, other] == 5.0)
+    # value columns only (the scoring pass when no block is always computed)
+    vonly = torch.zeros((slots, H, S, dh), dtype=td, device=DEV)
+    wd = to_device(w, dtype)
+    bd = to_device(bias, "f32")
+    B.k_qkv(dtype, to_device(a, dtype), wd[2 * D:], bd[2 * D:], D, H, S, S, v_cache=vonly,
+            n_offset=2 * D, n_cols=D)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(_host(vonly), _host(vc))
+
+
+# --------------------------------------------------------------------------
+# Attention (Eq. 3), dense and partial
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("S,dh,H,per", [(64, 64, 2, 64), (100, 64, 2, 100), (320, 64, 3, 50),
+                                        (320, 80, 2, 32), (131, 16, 2, 131), (1088, 64, 1, 218),
+                                        (70, 128, 1, 5), (200, 48, 2, 1)])
+def test_attention(dtype, S, dh, H, per):
+    slots = 2
+    D = H * dh
+    q = normal_rows((slots * per, D), seed=51, dtype=dtype)
+    k = normal_rows((slots, H, S, dh), seed=52, dtype=dtype)
+    v = normal_rows((slots, H, S, dh), seed=53, dtype=dtype)
+    td = to_device(q[:1], dtype).dtype
+    out = torch.empty((slots * per, D), dtype=td, device=DEV)
+    B.k_attention(dtype, to_device(q, dtype), to_device(k, dtype), to_device(v, dtype), out, slots, H, S, dh, per)
+    torch.cuda.synchronize()
+    ref = np.empty((slots * per, D))
+    for s in range(slots):
+        for h in range(H):
+            ref[s * per:(s + 1) * per, h * dh:(h + 1) * dh] = O.attention(
+                q[s * per:(s + 1) * per, h * dh:(h + 1) * dh], k[s, h], v[s, h])
+    _close(out, ref, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_attention_query_rows_independent(dtype):
+    """A query's result does not depend on the other queries of the launch:
+    the partial launch reproduces the dense launch's rows bit for bit."""
+    slots, H, S, dh = 2, 2, 200, 64
+    D = H * dh
+    q = normal_rows((slots * S, D), seed=54, dtype=dtype)
+    k = normal_rows((slots, H, S, dh), seed=55, dtype=dtype)
+    v = normal_rows((slots, H, S, dh), seed=56, dtype=dtype)
+    kd, vd = to_device(k, dtype), to_device(v, dtype)
+    td = kd.dtype
+    dense = torch.empty((slots * S, D), dtype=td, device=DEV)
+    B.k_attention(dtype, to_device(q, dtype), kd, vd, dense, slots, H, S, dh, S)
+    N = 37
+    idx = random_index_sets(slots, S, N, seed=57)
+    qs = np.concatenate([q[s * S + idx[s]] for s in range(slots)])
+    part = torch.empty((slots * N, D), dtype=td, device=DEV)
+    B.k_attention(dtype, to_device(qs, dtype), kd, vd, part, slots, H, S, dh, N)
+    torch.cuda.synchronize()
+    dh_ = _host(dense)
+    want = np.concatenate([dh_[s * S + idx[s]] for s in range(slots)])
+    np.testing.assert_array_equal(_host(part), want)
+
+
+# --------------------------------------------------------------------------
+# Eq. (8): scores and selection
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("slots,H,S,dh", [(2, 12, 320, 64), (3, 16, 100, 80), (1, 1, 7, 16)])
+def test_scores_bitwise(dtype, slots, H, S, dh):
+    v = normal_rows((slots, H, S, dh), seed=61, dtype=dtype)
+    r = to_storage(v + normal_rows((slots, H, S, dh), seed=62, std=0.3), dtype)
+    r[0, :, 1] = v[0, :, 1]          # identical row: score exactly 1
+    if S > 4:
+        r[0, :, 2] = 0.0              # one zero row: score 0
+        v[0, :, 3] = 0.0
+        r[0, :, 3] = 0.0              # both zero: score 1
+    vd, rd = to_device(v, dtype), to_device(r, dtype)
+    scores = torch.empty((slots, S), dtype=torch.float64, device=DEV)
+    B.k_scores(dtype, vd, rd, scores, update_ref=True)
+    torch.cuda.synchronize()
+    rows = lambda a: a.transpose(0, 2, 1, 3).reshape(slots, S, H * dh)  # noqa: E731
+    want = O.cosine_scores(rows(v), rows(r))
+    got = scores.cpu().numpy()
+    np.testing.assert_array_equal(got, want)
+    assert got[0, 1] == 1.0
+    np.testing.assert_array_equal(_host(rd), v)   # the reference now holds v
+
+
+@pytest.mark.parametrize("slots,S,n", [(4, 320, 50), (2, 320, 0), (2, 320, 320), (1, 1, 1), (3, 1088, 218),
+                                       (2, 4096, 1000), (5, 33, 31)])
+def test_select_bit_exact(slots, S, n):
+    g = np.random.Generator(np.random.Philox(71))
+    s = 1.0 - np.abs(g.standard_normal((slots, S))) * 1e-3
+    s[0, : S // 3] = np.round(s[0, : S // 3], 4)   # many exact ties
+    if S > 10:
+        s[-1, 5] = np.nan
+        s[-1, 6] = -0.0
+        s[-1, 7] = 0.0
+    idx = torch.full((slots, n), -1, dtype=torch.int32, device=DEV)
+    B.k_select(torch.from_numpy(s).to(DEV), n, idx)
+    torch.cuda.synchronize()
+    want = np.stack([O.select_least_similar(s[b], n) for b in range(slots)])
+    np.testing.assert_array_equal(idx.cpu().numpy(), want)

@@ -1,0 +1,69 @@
+"""Host-side checks of the HIP library that need no GPU: it loads, exports
+every symbol its headers declare, sizes workspaces, and rejects bad
+arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2503_12450_amd import binding as B
+from paper_2503_12450_amd.workload import WORKLOADS, MarDims
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for h in ("mar_cache.h", "mar_kernels.h"):
+        text = open(os.path.join(ROOT, "include", h)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b(mar_[a-z_]+)\s*\(", text))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.load()
+    declared = _declared()
+    assert declared == set(B.EXPORTED)
+    for name in declared:
+        assert getattr(lib, name) is not None
+
+
+def test_workspace_bytes_for_every_workload():
+    for key, w in WORKLOADS.items():
+        n = B.workspace_bytes(w.dims)
+        d = w.dims
+        es = 2 if d.dtype == "bf16" else 4
+        cache = (d.n_layers - d.full_prefix) * 2 * d.max_slots * d.seq_len * d.d_model * es
+        assert n > cache, key
+        assert n % 256 == 0
+
+
+@pytest.mark.parametrize("bad", [
+    dict(d_model=100), dict(n_heads=7), dict(d_mlp=100), dict(seq_len=0), dict(seq_len=5000),
+    dict(max_slots=0), dict(full_prefix=4), dict(full_prefix=-1), dict(n_layers=0),
+    dict(d_model=1152, n_heads=8),   # d_head 144 > 128
+    dict(d_model=192, n_heads=16),   # d_head 12 not a multiple of 16
+])
+def test_workspace_rejects_unsupported_dims(bad):
+    base = dict(n_layers=4, d_model=256, n_heads=4, d_mlp=1024, seq_len=64, max_slots=2,
+                full_prefix=2, dtype="bf16")
+    base.update(bad)
+    with pytest.raises(B.MarError) as e:
+        B.workspace_bytes(MarDims(**base))
+    assert e.value.status == B.MAR_E_SHAPE
+
+
+def test_host_checks_run_before_any_device_call():
+    lib = B.load()
+    d = B.dims_c(WORKLOADS["block-f32"].dims)
+    h = ctypes.c_void_p()
+    assert lib.mar_cache_init(ctypes.byref(d), None, None, 0, None, ctypes.byref(h)) == B.MAR_E_ARG
+    assert b"blocks" in lib.mar_last_error()
+    assert lib.mar_step(None, None, None, 0, 1, 0, 0, None, None) == B.MAR_E_ARG
+    assert lib.mar_cfg_combine(None, None, None, 0, 1, 0, 1.0, None, None, None) == B.MAR_E_ARG
+    assert lib.mar_k_select(None, 1, 8, 2, None, None) == B.MAR_E_ARG
+    assert lib.mar_k_attention(1, 16, 16, 16, 16, 1, 1, 8, 24, 8, None) == B.MAR_E_SHAPE
+    assert lib.mar_cache_destroy(None) == B.MAR_OK
+    assert lib.mar_output(None) is None

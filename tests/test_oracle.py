@@ -179,6 +179,19 @@ def test_cosine_matches_scipy_and_closed_forms():
     assert list(cosine_scores(o, z)) == [0.0, 0.0]
 
 
+def test_cosine_dot_products_are_exactly_rounded():
+    from fractions import Fraction
+    rng = np.random.default_rng(21)
+    v = storage_round(rng.standard_normal((6, 257)) * np.exp(rng.uniform(-12, 4, (6, 257))), "bf16")
+    r = storage_round(v + rng.standard_normal((6, 257)), "bf16")
+    s = cosine_scores(v, r)
+    for i in range(6):
+        dot = float(sum(Fraction(a) * Fraction(b) for a, b in zip(v[i], r[i])))
+        nv = float(sum(Fraction(a) * Fraction(a) for a in v[i]))
+        nr = float(sum(Fraction(b) * Fraction(b) for b in r[i]))
+        assert s[i] == dot / math.sqrt(nv * nr)
+
+
 def test_cosine_bf16_self_identity():
     # scoring a stored row against itself gives exactly 1 in fp64
     v = storage_round(np.random.default_rng(2).standard_normal((64, 1024)), "bf16")
