@@ -11,8 +11,9 @@
  * Row mapping used below: with `idx` given, row m of a compact matrix belongs
  * to slot m / per_slot and token idx[m] of that slot; without it, row m is
  * token m % per_slot of slot m / per_slot (and per_slot must equal seq).
- * A cache layout [slots, H, seq, d_head] holds one slot's keys (or values)
- * of head h as a contiguous seq x d_head block.
+ * The key cache [slots, H, seq, d_head] holds one slot's keys of head h as a
+ * contiguous seq x d_head block; the value cache [slots, H, d_head, seq]
+ * holds the values transposed (one row per dimension, tokens along it).
  */
 #ifndef MAR_KERNELS_H
 #define MAR_KERNELS_H
@@ -56,9 +57,11 @@ mar_status mar_k_linear_residual(int32_t dtype, const void* a, const void* w, co
  * computed rows replace their cached keys and values).  Columns
  * [n_offset, n_offset + n_cols) of the stacked [3D, D] projection, with w
  * and bias pointing at column n_offset:
- *   query columns  -> q_out[m, c]                 ([m, D], dtype)
- *   key columns    -> k_cache[slot, head, tok, :] ([slots, H, seq, dh])
- *   value columns  -> v_cache[...] and v_copy[...] (nullable)
+ *   query columns  -> q_out[m, c]                  ([m, D], dtype)
+ *   key columns    -> k_cache[slot, head, tok, :]  ([slots, H, seq, dh])
+ *   value columns  -> v_cache[slot, head, :, tok]  ([slots, H, dh, seq],
+ *                     transposed; nullable) and v_copy[slot, head, tok, :]
+ *                     ([slots, H, seq, dh]; nullable); one of them required
  * slot/tok from the row mapping.  d_model % 64 == 0. */
 mar_status mar_k_qkv(int32_t dtype, const void* a, const void* w, const float* bias, int32_t m,
                      int32_t n_cols, int32_t n_offset, int32_t d_model, int32_t n_heads, int32_t seq,
@@ -67,7 +70,8 @@ mar_status mar_k_qkv(int32_t dtype, const void* a, const void* w, const float* b
 
 /* Eq. (3) without mask for per_slot query rows per slot against all seq
  * keys of the slot: q, out [n_slots * per_slot, H * d_head] (head h at
- * columns h * d_head ...), k, v [n_slots, H, seq, d_head].  Scale
+ * columns h * d_head ...), k [n_slots, H, seq, d_head], v transposed
+ * [n_slots, H, d_head, seq] (the value cache layout).  Scale
  * 1/sqrt(d_head); softmax statistics in fp32.  d_head in {16, 32, ..., 128}.
  * per_slot == seq is the dense block; per_slot = N the cached one. */
 mar_status mar_k_attention(int32_t dtype, const void* q, const void* k, const void* v, void* out,
@@ -87,6 +91,14 @@ mar_status mar_k_scores(int32_t dtype, const void* v_cur, void* v_ref, int32_t n
  * seq <= 4096. */
 mar_status mar_k_select(const double* scores, int32_t n_slots, int32_t seq, int32_t n, int32_t* idx,
                         void* stream);
+
+/* Tuning hook: force tile configuration `variant` (0 .. MAR_GEMM_VARIANTS-1)
+ * for every later matrix product of the process, or -1 to restore the
+ * choice by shape.  Every configuration uses the same MFMA instruction and
+ * visits k in the same order, so results do not change by a single bit.
+ * Not thread-safe with concurrent launches. */
+#define MAR_GEMM_VARIANTS 5
+mar_status mar_k_gemm_variant(int32_t variant);
 
 #ifdef __cplusplus
 }

@@ -29,8 +29,9 @@ EXPORTED = (
     "mar_workspace_bytes", "mar_cache_init", "mar_step", "mar_cfg_combine", "mar_output",
     "mar_cache_destroy", "mar_last_error", "mar_profile_start", "mar_profile_stop",
     "mar_k_layernorm", "mar_k_linear", "mar_k_linear_residual", "mar_k_qkv",
-    "mar_k_attention", "mar_k_scores", "mar_k_select",
+    "mar_k_attention", "mar_k_scores", "mar_k_select", "mar_k_gemm_variant",
 )
+GEMM_VARIANTS = 5
 
 
 class MarError(RuntimeError):
@@ -77,6 +78,7 @@ _SIGNATURES = {
     "mar_k_attention": (_i32, [_i32, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp]),
     "mar_k_scores": (_i32, [_i32, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _i32, _vp]),
     "mar_k_select": (_i32, [_vp, _i32, _i32, _i32, _vp, _vp]),
+    "mar_k_gemm_variant": (_i32, [_i32]),
 }
 
 _lib: Optional[ctypes.CDLL] = None
@@ -275,3 +277,8 @@ def k_scores(dtype: str, v_cur, v_ref, scores, update_ref: bool = False, stream=
 def k_select(scores, n: int, idx, stream=None) -> None:
     n_slots, seq = scores.shape
     _check(load().mar_k_select(scores.data_ptr(), n_slots, seq, n, idx.data_ptr(), _stream(stream)))
+
+
+def k_gemm_variant(variant: int) -> None:
+    """Force a tile configuration of the matrix products (-1: by shape)."""
+    _check(load().mar_k_gemm_variant(variant))

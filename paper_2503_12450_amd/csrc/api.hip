@@ -511,10 +511,11 @@ mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0, in
 
   if (mode == MAR_FULL) {
     for (int l = 0; l < c.L; ++l) {
+      // keys [slot, head, token, d]; values transposed for attention, and as
+      // token rows into the scoring reference at the scoring block
       void* kd = l >= c.P ? offset<void>(cache->layers[l].kc, slot_off, c.es) : ktmp;
-      void* vd = l >= c.P ? offset<void>(cache->layers[l].vc, slot_off, c.es)
-                          : (l == score_layer ? vref : vtmp);
-      void* vcopy = (l == score_layer && l >= c.P) ? vref : nullptr;
+      void* vd = l >= c.P ? offset<void>(cache->layers[l].vc, slot_off, c.es) : vtmp;
+      void* vcopy = l == score_layer ? vref : nullptr;
       s = dense_block(c, l, l == 0, x, kd, vd, vcopy, l == c.L - 1 ? Yslot : nullptr);
       if (s != MAR_OK) return s;
     }
@@ -539,14 +540,15 @@ mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0, in
       e.d_head = c.dh;
       e.seq = S;
       e.per_slot = S;
-      e.v_cache = vcur;
+      e.v_cache = nullptr;  // value rows only, untransposed, for scoring
+      e.v_copy = vcur;
       const void* wv = offset<const void>(w.qkv_w, 2L * c.D * c.D, c.es);
       TIMED(MAR_PROF_QKV, 2.0 * Mfull * c.D * c.D,
             gemm_bytes(Mfull, c.D, c.D, static_cast<double>(c.es), static_cast<double>(c.es), false),
             launch_gemm(c.dtype, a, wv, Mfull, c.D, c.D, e, c.st), "value gemm");
     } else {
       for (int l = 0; l < c.P; ++l) {
-        s = dense_block(c, l, l == 0, x, ktmp, l == score_layer ? vcur : vtmp, nullptr, nullptr);
+        s = dense_block(c, l, l == 0, x, ktmp, vtmp, l == score_layer ? vcur : nullptr, nullptr);
         if (s != MAR_OK) return s;
       }
     }
@@ -732,7 +734,7 @@ mar_status mar_k_qkv(int32_t dtype, const void* a, const void* w, const float* b
   if (per_slot < 1 || seq < 1 || (!idx && per_slot != seq)) return fail(MAR_E_SHAPE, "bad row mapping");
   const bool has_q = n_offset < d_model, has_k = n_offset < 2 * d_model && n_offset + n_cols > d_model,
              has_v = n_offset + n_cols > 2 * d_model;
-  if ((has_q && !q_out) || (has_k && !k_cache) || (has_v && !v_cache))
+  if ((has_q && !q_out) || (has_k && !k_cache) || (has_v && !v_cache && !v_copy))
     return fail(MAR_E_ARG, "missing output for the requested columns");
   if (!aligned16(a) || !aligned16(w)) return fail(MAR_E_ARG, "operands must be 16-byte aligned");
   EpiArgs e{};
@@ -789,6 +791,13 @@ mar_status mar_k_select(const double* scores, int32_t n_slots, int32_t seq, int3
   if (!scores || (!idx && n > 0 && n_slots > 0)) return fail(MAR_E_ARG, "NULL pointer");
   if (n_slots < 0 || seq < 1 || seq > kMaxSeq || n < 0 || n > seq) return fail(MAR_E_SHAPE, "bad sizes");
   MAR_HIP(launch_select(scores, n_slots, seq, n, idx, static_cast<hipStream_t>(stream)), "select");
+  return MAR_OK;
+}
+
+mar_status mar_k_gemm_variant(int32_t variant) {
+  g_err.clear();
+  if (variant < -1 || variant >= MAR_GEMM_VARIANTS) return fail(MAR_E_ARG, "unknown variant %d", variant);
+  set_gemm_variant(variant);
   return MAR_OK;
 }
 

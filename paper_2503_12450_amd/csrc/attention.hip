@@ -3,15 +3,12 @@
 // is a query) and partial for the cached blocks (the N selected rows are the
 // queries, keys/values of every token come from the per-block cache).
 //
-// bf16 path, one workgroup per (slot, head, 64 queries), 16 queries per
-// wave.  Keys/values stream through LDS in tiles of 64 keys with an online
-// softmax, so any sequence length works.  With 16x16x32 bf16 MFMAs:
-//   S^T (keys x queries) = K Q^T          A = K tile rows, B = this wave's Q
-//   O^T (d x queries)   += V^T P^T        A = V tile read transposed from
-//                                         LDS, B = P straight from the
-//                                         registers that produced S^T
-// Computing the transposed products keeps every query in one column, so a
-// lane owns a query's softmax statistics and its output column; the sum over
+// bf16 path: one workgroup per (slot, head, 64 queries); keys/values stream
+// through LDS in blocks of 64 keys with an online softmax, so any sequence
+// length works.  The products are the transposed ones (S^T = K Q^T,
+// O^T = V^T P^T) so that every query stays in one MFMA column: a lane then
+// owns a query's softmax statistics and output, and the probabilities feed
+// the second product from the registers that produced them.  The sum over
 // keys in the second product visits each lane's keys in a permuted order,
 // which only relabels the reduction index.  A query's result depends only on
 // its own row and the slot's keys/values, so a query computed in a partial
@@ -25,162 +22,205 @@ namespace marcache {
 constexpr int kKeyTile = 64;
 constexpr float kLog2e = 1.4426950408889634f;
 
-template <int DH>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict__ Q,
-                                                        const bf16_t* __restrict__ Kc,
-                                                        const bf16_t* __restrict__ Vc,
-                                                        bf16_t* __restrict__ O, int H, int seq,
-                                                        int per_slot, float scale_log2) {
-  constexpr int DC = (DH + 31) / 32;   // 32-wide d chunks of the first product
-  constexpr int DT = DH / 16;          // 16-wide d tiles of the output
-  constexpr int KROW = DH + 8;         // padded K row (elements)
-  constexpr int VROW = kKeyTile + 8;   // padded V^T row (elements)
-  __shared__ __align__(16) bf16_t Ks[kKeyTile * KROW];
-  __shared__ __align__(16) bf16_t Vt[DH * VROW];
+// bf16: WAVES waves of 32 queries per workgroup; keys and transposed values
+// (V^T, [d][key] per slot and head) stream through LDS in blocks of 64 keys.
+// Per block and wave, with 32x32x16 MFMAs:
+//   S^T (32 keys x 32 queries) = K Q^T   A = K rows from LDS, B = Q (registers)
+//   O^T (32 d x 32 queries)   += V^T P^T A = V^T rows from LDS, B = P (registers)
+// Lane (q, h) = (lane % 32, lane / 32) owns query q: S^T gives it keys
+// 8 j + 4 h + i (j, i = 0..3) of each 32-key half, which are exactly the
+// eight k-slots it feeds to the second product for each 16-key step (in a
+// permuted key order that the V^T operand follows), and O^T gives it rows
+// d = 8 j + 4 h + i of its query's output.  The softmax statistics of a
+// query live in its two lanes (q and q + 32).
+template <int DH, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __restrict__ Q,
+                                                               const bf16_t* __restrict__ Kc,
+                                                               const bf16_t* __restrict__ Vc,
+                                                               bf16_t* __restrict__ O, int H, int seq,
+                                                               int per_slot, float scale_log2) {
+  constexpr int KB = 64;               // keys per LDS block
+  constexpr int DS = DH / 16;          // k-steps of S^T
+  constexpr int DT = (DH + 31) / 32;   // 32-row tiles of O^T
+  constexpr int DHP = DT * 32;         // V^T rows incl. zero padding
+  constexpr int KROW = DH + 8;         // K row stride (elements)
+  constexpr int VROW = KB + 4;         // V^T row stride: 136 bytes, conflict-free 8-byte reads
+  constexpr int THREADS = 64 * WAVES;
+  constexpr int QB = 32 * WAVES;
+  __shared__ __align__(16) bf16_t Ks[KB * KROW];
+  __shared__ __align__(16) bf16_t Vt[DHP * VROW];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int qblocks = (per_slot + 63) / 64;
+  const int qblocks = (per_slot + QB - 1) / QB;
   const int qb = blockIdx.x % qblocks;
   const int bh = blockIdx.x / qblocks;
   const int h = bh % H;
   const int b = bh / H;
   const int D = H * DH;
-
-  const int ql = lane & 15;   // this lane's query within the wave
-  const int g = lane >> 4;    // lane group 0..3
-  const int qi = qb * 64 + wave * 16 + ql;
+  const int ql = lane & 31;
+  const int hg = lane >> 5;
+  const int qi = qb * QB + wave * 32 + ql;
   const bool q_ok = qi < per_slot;
   const long q_row = static_cast<long>(b) * per_slot + qi;
 
-  // B operand of S^T = K Q^T: Q[q][32 c + 8 g .. + 7]
-  u32x4_t qf[DC];
+  u32x4_t qf[DS];  // Q[q][16 s + 8 hg .. + 7]
 #pragma unroll
-  for (int c = 0; c < DC; ++c) {
-    const int d0 = 32 * c + 8 * g;
-    if (q_ok && d0 < DH)
-      qf[c] = *reinterpret_cast<const u32x4_t*>(Q + q_row * D + h * DH + d0);
-    else
-      qf[c] = u32x4_t{0u, 0u, 0u, 0u};
+  for (int st = 0; st < DS; ++st)
+    qf[st] = q_ok ? *reinterpret_cast<const u32x4_t*>(Q + q_row * D + h * DH + 16 * st + 8 * hg)
+                  : u32x4_t{0u, 0u, 0u, 0u};
+  if constexpr (DHP > DH) {
+    for (int i = tid; i < (DHP - DH) * VROW; i += THREADS) Vt[DH * VROW + i] = 0;
   }
 
   const bf16_t* kbase = Kc + (static_cast<long>(b) * H + h) * seq * DH;
-  const bf16_t* vbase = Vc + (static_cast<long>(b) * H + h) * seq * DH;
-
-  f32x4_t oacc[DT];
+  const bf16_t* vbase = Vc + (static_cast<long>(b) * H + h) * seq * DH;  // [DH][seq]
+  f32x16_t oacc[DT];
 #pragma unroll
-  for (int t = 0; t < DT; ++t) oacc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < DT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[t][r] = 0.f;
   float m_run = -__builtin_huge_valf();
   float l_run = 0.f;  // this lane's share of the row sum
 
-  constexpr int VEC_PER_ROW = DH / 8;
-  constexpr int TILE_VECS = kKeyTile * VEC_PER_ROW;
-  const int n_tiles = (seq + kKeyTile - 1) / kKeyTile;
-  for (int kt = 0; kt < n_tiles; ++kt) {
-    const int key0 = kt * kKeyTile;
-    __syncthreads();  // previous tile fully consumed
-    for (int v = tid; v < TILE_VECS; v += 256) {
-      const int r = v / VEC_PER_ROW;
-      const int c = v - r * VEC_PER_ROW;
+  // A block is KB key rows of K (DH / 8 chunks of 16 bytes each) and DH rows
+  // of V^T (KB / 8 chunks each): DH / 16 chunks of each per thread.  The next
+  // block is loaded into registers while the current one is multiplied.
+  constexpr int CH = DH / 8;
+  constexpr int PER_T = DH / 16;
+  static_assert(PER_T * THREADS == KB * CH && PER_T * THREADS == DH * (KB / 8), "block/threads");
+  const bool vec_v = (seq & 7) == 0;  // V^T rows 16-byte aligned
+  u32x4_t rk[PER_T], rv[PER_T];
+  auto load_block = [&](int key0) {
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      const int v = tid + THREADS * i;
+      const int r = v / CH, c = v - (v / CH) * CH;
       const int key = key0 + r;
-      u32x4_t kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
-      if (key < seq) {
-        kv = *reinterpret_cast<const u32x4_t*>(kbase + static_cast<long>(key) * DH + c * 8);
-        vv = *reinterpret_cast<const u32x4_t*>(vbase + static_cast<long>(key) * DH + c * 8);
-      }
-      *reinterpret_cast<u32x4_t*>(Ks + r * KROW + c * 8) = kv;
+      rk[i] = key < seq ? *reinterpret_cast<const u32x4_t*>(kbase + static_cast<long>(key) * DH + 8 * c)
+                        : u32x4_t{0u, 0u, 0u, 0u};
+      const int d = v >> 3, k8 = key0 + 8 * (v & 7);
+      const bf16_t* src = vbase + static_cast<long>(d) * seq + k8;
+      if (vec_v && k8 + 8 <= seq) {
+        rv[i] = *reinterpret_cast<const u32x4_t*>(src);
+      } else {
+        uint32_t w[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        Vt[(c * 8 + 2 * i) * VROW + r] = static_cast<bf16_t>(vv[i] & 0xFFFFu);
-        Vt[(c * 8 + 2 * i + 1) * VROW + r] = static_cast<bf16_t>(vv[i] >> 16);
+        for (int e2 = 0; e2 < 4; ++e2) {
+          const uint32_t lo = k8 + 2 * e2 < seq ? src[2 * e2] : 0u;
+          const uint32_t hi = k8 + 2 * e2 + 1 < seq ? src[2 * e2 + 1] : 0u;
+          w[e2] = lo | (hi << 16);
+        }
+        rv[i] = u32x4_t{w[0], w[1], w[2], w[3]};
       }
     }
-    __syncthreads();
+  };
+  auto store_block = [&]() {
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      const int v = tid + THREADS * i;
+      const int r = v / CH, c = v - (v / CH) * CH;
+      *reinterpret_cast<u32x4_t*>(Ks + r * KROW + 8 * c) = rk[i];
+      const int d = v >> 3, c8 = v & 7;
+      u32x2_t* dst = reinterpret_cast<u32x2_t*>(Vt + d * VROW + 8 * c8);
+      dst[0] = u32x2_t{rv[i][0], rv[i][1]};
+      dst[1] = u32x2_t{rv[i][2], rv[i][3]};
+    }
+  };
 
-    // S^T for 4 subtiles of 16 keys: s[j][i] = key 16 j + 4 g + i, query ql
-    f32x4_t s[4];
+  const int n_blocks = (seq + KB - 1) / KB;
+  load_block(0);
+  for (int kb = 0; kb < n_blocks; ++kb) {
+    const int key0 = kb * KB;
+    __syncthreads();  // the previous block is consumed
+    store_block();
+    __syncthreads();
+    if (kb + 1 < n_blocks) load_block(key0 + KB);
+
+    f32x16_t sc[2];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      s[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int sb = 0; sb < 2; ++sb) {
 #pragma unroll
-      for (int c = 0; c < DC; ++c) {
-        const int d0 = 32 * c + 8 * g;
-        u32x4_t kf = {0u, 0u, 0u, 0u};
-        if (d0 < DH) kf = *reinterpret_cast<const u32x4_t*>(Ks + (16 * j + ql) * KROW + d0);
-        s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kf),
-                                                       __builtin_bit_cast(bf16x8_t, qf[c]),
-                                                       s[j], 0, 0, 0);
+      for (int r = 0; r < 16; ++r) sc[sb][r] = 0.f;
+#pragma unroll
+      for (int st = 0; st < DS; ++st) {
+        const u32x4_t kf = *reinterpret_cast<const u32x4_t*>(Ks + (32 * sb + ql) * KROW + 16 * st + 8 * hg);
+        sc[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf),
+                                                         __builtin_bit_cast(bf16x8_t, qf[st]), sc[sb], 0, 0, 0);
       }
     }
-    // scale, mask, tile max of this query across its four lanes
+    // scale, mask keys past the end, block max of this query over its two lanes
     float tmax = -__builtin_huge_valf();
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = key0 + 16 * j + 4 * g + i;
-        const float x = (key < seq) ? s[j][i] * scale_log2 : -__builtin_huge_valf();
-        s[j][i] = x;
+      for (int r = 0; r < 16; ++r) {
+        const int key = key0 + 32 * sb + 8 * (r >> 2) + 4 * hg + (r & 3);
+        const float x = key < seq ? sc[sb][r] * scale_log2 : -__builtin_huge_valf();
+        sc[sb][r] = x;
         tmax = fmaxf(tmax, x);
       }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
     const float m_new = fmaxf(m_run, tmax);
     const float alpha = exp2f(m_run - m_new);
     m_run = m_new;
     float psum = 0.f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float p = exp2f(s[j][i] - m_new);
-        s[j][i] = p;
+      for (int r = 0; r < 16; ++r) {
+        const float p = exp2f(sc[sb][r] - m_new);
+        sc[sb][r] = p;
         psum += p;
       }
     l_run = l_run * alpha + psum;
 #pragma unroll
     for (int t = 0; t < DT; ++t)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) oacc[t][i] *= alpha;
+      for (int r = 0; r < 16; ++r) oacc[t][r] *= alpha;
 
-    // O^T += V^T P^T over two 32-key chunks; this lane's k-slots are keys
-    // {32 c + 4 g + i} and {32 c + 16 + 4 g + i}, i = 0..3
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      u32x4_t pf;
-      pf[0] = pack2bf(s[2 * c][0], s[2 * c][1]);
-      pf[1] = pack2bf(s[2 * c][2], s[2 * c][3]);
-      pf[2] = pack2bf(s[2 * c + 1][0], s[2 * c + 1][1]);
-      pf[3] = pack2bf(s[2 * c + 1][2], s[2 * c + 1][3]);
+    for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-      for (int t = 0; t < DT; ++t) {
-        const bf16_t* vr = Vt + (16 * t + ql) * VROW + 32 * c + 4 * g;
-        const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vr);
-        const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vr + 16);
-        const u32x4_t vf = {lo[0], lo[1], hi[0], hi[1]};
-        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vf),
-                                                          __builtin_bit_cast(bf16x8_t, pf),
-                                                          oacc[t], 0, 0, 0);
+      for (int s2 = 0; s2 < 2; ++s2) {
+        u32x4_t pf;  // keys 32 sb + 16 s2 + {4 hg + i, 8 + 4 hg + i}
+        pf[0] = pack2bf(sc[sb][8 * s2 + 0], sc[sb][8 * s2 + 1]);
+        pf[1] = pack2bf(sc[sb][8 * s2 + 2], sc[sb][8 * s2 + 3]);
+        pf[2] = pack2bf(sc[sb][8 * s2 + 4], sc[sb][8 * s2 + 5]);
+        pf[3] = pack2bf(sc[sb][8 * s2 + 6], sc[sb][8 * s2 + 7]);
+#pragma unroll
+        for (int t = 0; t < DT; ++t) {
+          const bf16_t* vr = Vt + (32 * t + ql) * VROW + 32 * sb + 16 * s2 + 4 * hg;
+          const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vr);
+          const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vr + 8);
+          const u32x4_t vf = {lo[0], lo[1], hi[0], hi[1]};
+          oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vf),
+                                                            __builtin_bit_cast(bf16x8_t, pf), oacc[t], 0, 0, 0);
+        }
       }
-    }
   }
 
-  float l_tot = l_run + __shfl_xor(l_run, 16, 64);
-  l_tot += __shfl_xor(l_tot, 32, 64);
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if (!q_ok) return;
   const float inv = 1.0f / l_tot;
-  // oacc[t][i] = O[query ql][d = 16 t + 4 g + i]
+  // oacc[t][4 j + i] = O[query][d = 32 t + 8 j + 4 hg + i]
 #pragma unroll
-  for (int t = 0; t < DT; ++t) {
-    u32x2_t w;
-    w[0] = pack2bf(oacc[t][0] * inv, oacc[t][1] * inv);
-    w[1] = pack2bf(oacc[t][2] * inv, oacc[t][3] * inv);
-    *reinterpret_cast<u32x2_t*>(O + q_row * D + h * DH + 16 * t + 4 * g) = w;
-  }
+  for (int t = 0; t < DT; ++t)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int d0 = 32 * t + 8 * j + 4 * hg;
+      if (d0 < DH) {
+        u32x2_t w;
+        w[0] = pack2bf(oacc[t][4 * j] * inv, oacc[t][4 * j + 1] * inv);
+        w[1] = pack2bf(oacc[t][4 * j + 2] * inv, oacc[t][4 * j + 3] * inv);
+        *reinterpret_cast<u32x2_t*>(O + q_row * D + h * DH + d0) = w;
+      }
+    }
 }
 
-// fp32: 64 queries per workgroup, one per lane; keys/values tiled in LDS.
+// fp32: 64 queries per workgroup, one per lane; keys and transposed values
+// tiled in LDS.
 template <int DH>
 __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ Q,
                                                       const float* __restrict__ Kc,
@@ -188,7 +228,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
                                                       float* __restrict__ O, int H, int seq,
                                                       int per_slot, float scale_log2) {
   __shared__ float Ks[kKeyTile * DH];
-  __shared__ float Vs[kKeyTile * DH];
+  __shared__ float Vt[DH * kKeyTile];
   const int lane = threadIdx.x;
   const int qblocks = (per_slot + 63) / 64;
   const int qb = blockIdx.x % qblocks;
@@ -206,28 +246,29 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
     acc[d] = 0.f;
   }
   const float* kbase = Kc + (static_cast<long>(b) * H + h) * seq * DH;
-  const float* vbase = Vc + (static_cast<long>(b) * H + h) * seq * DH;
+  const float* vbase = Vc + (static_cast<long>(b) * H + h) * seq * DH;  // [DH][seq]
   float m_run = -__builtin_huge_valf(), l_run = 0.f;
   for (int key0 = 0; key0 < seq; key0 += kKeyTile) {
     const int nk = min(kKeyTile, seq - key0);
     __syncthreads();
-    for (int e = lane; e < nk * DH; e += 64) {
-      Ks[e] = kbase[static_cast<long>(key0) * DH + e];
-      Vs[e] = vbase[static_cast<long>(key0) * DH + e];
+    for (int e = lane; e < nk * DH; e += 64) Ks[e] = kbase[static_cast<long>(key0) * DH + e];
+    for (int e = lane; e < DH * kKeyTile; e += 64) {
+      const int d = e / kKeyTile, j = e - d * kKeyTile;
+      Vt[e] = j < nk ? vbase[static_cast<long>(d) * seq + key0 + j] : 0.f;
     }
     __syncthreads();
     for (int j = 0; j < nk; ++j) {
-      float s = 0.f;
+      float sdot = 0.f;
 #pragma unroll
-      for (int d = 0; d < DH; ++d) s = fmaf(q[d], Ks[j * DH + d], s);
-      s *= scale_log2;
-      const float m_new = fmaxf(m_run, s);
+      for (int d = 0; d < DH; ++d) sdot = fmaf(q[d], Ks[j * DH + d], sdot);
+      sdot *= scale_log2;
+      const float m_new = fmaxf(m_run, sdot);
       const float alpha = exp2f(m_run - m_new);
-      const float p = exp2f(s - m_new);
+      const float p = exp2f(sdot - m_new);
       m_run = m_new;
       l_run = l_run * alpha + p;
 #pragma unroll
-      for (int d = 0; d < DH; ++d) acc[d] = fmaf(p, Vs[j * DH + d], acc[d] * alpha);
+      for (int d = 0; d < DH; ++d) acc[d] = fmaf(p, Vt[d * kKeyTile + j], acc[d] * alpha);
     }
   }
   if (!q_ok) return;
@@ -239,15 +280,18 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 template <int DH>
 static hipError_t attn_launch(int dtype, const void* q, const void* k, const void* v, void* out,
                               int n_slots, int H, int seq, int per_slot, hipStream_t st) {
-  const int qblocks = (per_slot + 63) / 64;
-  const long grid = static_cast<long>(n_slots) * H * qblocks;
   const float scale_log2 = kLog2e / sqrtf(static_cast<float>(DH));
   if (dtype == DT_BF16) {
-    hipLaunchKernelGGL(attn_bf16_kernel<DH>, dim3(static_cast<unsigned>(grid)), dim3(256), 0, st,
+    constexpr int WAVES = 2;  // 64 queries per workgroup
+    const int qblocks = (per_slot + 32 * WAVES - 1) / (32 * WAVES);
+    const long grid = static_cast<long>(n_slots) * H * qblocks;
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, WAVES>), dim3(static_cast<unsigned>(grid)), dim3(64 * WAVES), 0, st,
                        static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
                        static_cast<const bf16_t*>(v), static_cast<bf16_t*>(out), H, seq,
                        per_slot, scale_log2);
   } else {
+    const int qblocks = (per_slot + 63) / 64;
+    const long grid = static_cast<long>(n_slots) * H * qblocks;
     hipLaunchKernelGGL(attn_f32_kernel<DH>, dim3(static_cast<unsigned>(grid)), dim3(64), 0, st,
                        static_cast<const float*>(q), static_cast<const float*>(k),
                        static_cast<const float*>(v), static_cast<float*>(out), H, seq, per_slot,

@@ -59,6 +59,27 @@ __device__ __forceinline__ uint32_t pack2bf(float lo, float hi) {
   return static_cast<uint32_t>(f2bf(lo)) | (static_cast<uint32_t>(f2bf(hi)) << 16);
 }
 
+// Exact division by a divisor d >= 2 fixed for the launch (Granlund &
+// Montgomery, "Division by invariant integers using multiplication", 1994):
+// with s = 31 + ceil(log2 d) >= 32 and magic = ceil(2^s / d) < 2^32,
+// floor(m / d) = (m * magic) >> s for every 0 <= m < 2^31.  d = 1 is
+// encoded as magic 0 (the identity).
+struct Divisor {
+  uint32_t magic;
+  int shift;  // s - 32
+};
+inline Divisor make_divisor(uint32_t d) {
+  if (d <= 1) return Divisor{0u, 0};
+  int l = 0;
+  while ((1ull << l) < d) ++l;
+  const int s = 31 + l;
+  const uint64_t magic = ((1ull << s) + d - 1) / d;
+  return Divisor{static_cast<uint32_t>(magic), s - 32};
+}
+__device__ __forceinline__ int div_by(int m, uint32_t magic, int shift) {
+  return magic ? static_cast<int>(__umulhi(static_cast<uint32_t>(m), magic) >> shift) : m;
+}
+
 // Butterfly sums across the 64 lanes of a wave; every lane gets the total.
 // The order of additions is fixed, so the result is deterministic.
 __device__ __forceinline__ float wave_sum(float v) {
@@ -105,23 +126,27 @@ struct EpiArgs {
   //   resid_copy (nullable) also receives the row at m.
   const int32_t* out_idx;
   float* resid_copy;
-  // QKV: n_global = n + n_offset selects q (< D), k (< 2D) or v; key/value
-  // rows go to cache[(slot * H + head) * seq + tok][d] with slot/tok from the
-  // row mapping (idx or dense).
+  // QKV: n_global = n + n_offset selects q (< D), k (< 2D) or v; keys go to
+  // k_cache[slot][head][tok][d], values to v_cache[slot][head][d][tok]
+  // (transposed), with slot/tok from the row mapping (idx or dense).
   int n_offset;
   int d_model, n_heads, d_head, seq, per_slot;
+  // m / per_slot = umulhi(m, slot_magic) >> slot_shift (set by launch_gemm)
+  uint32_t slot_magic;
+  int slot_shift;
   const int32_t* idx;
   void* k_cache;
   void* v_cache;
-  void* v_copy;  // nullable second destination of value rows (same layout)
+  void* v_copy;  // nullable: value rows again, untransposed [slot][head][tok][d]
 };
 
 hipError_t launch_gemm(int dtype, const void* A, const void* W, int M, int N, int K,
                        const EpiArgs& epi, hipStream_t st);
+void set_gemm_variant(int v);  // -1: by shape
 
 // Attention of per_slot queries per slot against the seq keys of the slot:
-// q, out [n_slots * per_slot, D] (head h at columns h*dh..); k, v
-// [n_slots, H, seq, dh].
+// q, out [n_slots * per_slot, D] (head h at columns h*dh..); k
+// [n_slots, H, seq, dh]; v transposed, [n_slots, H, dh, seq].
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v, void* out,
                             int n_slots, int H, int seq, int dh, int per_slot,
                             hipStream_t st);

@@ -2,13 +2,21 @@
 //
 // A [M, K] (activation rows, dense or compact selected rows) and W [N, K]
 // (nn.Linear layout) are both K-contiguous, which is what the MFMA operands
-// want: each lane feeds 16 bytes of consecutive k.  Tiles of BM x BN are
-// staged through LDS in BK-deep slices with a register prefetch of the next
-// slice (double-buffered LDS, one barrier per slice).  Four waves split the
-// tile 2 x 2; each wave issues 32x32 MFMAs:
+// want: each lane feeds 16 bytes of consecutive k.
+//
+// Data movement: each workgroup owns a BM x BN output tile and walks K in
+// slices of 128 bytes per row.  Slices are copied from HBM/L2 straight into
+// LDS by buffer loads with the LDS destination (no register staging), into
+// a ring of STAGES buffers: slice kt+STAGES-1 is in flight while slice kt is
+// multiplied.  Buffer descriptors cover only the tile's rows, so rows past M
+// (N) read as zeros without any masking.  Within a 128-byte row the eight
+// 16-byte chunks are XOR-swizzled by (row / 2) % 8, which spreads the 16
+// lanes of each LDS read phase over all 64 banks.
+//
+// Math: 32x32 MFMA tiles per wave,
 //   bf16: v_mfma_f32_32x32x16_bf16 (one per 16 k)
 //   fp32: v_mfma_f32_32x32x2_f32   (four per 8 k)
-// Accumulation is fp32.  Every output element sums its k in the same order
+// with fp32 accumulation.  Every output element sums its k in the same order
 // whatever the tile shape, M, or the row's position, so a row of a compact
 // (selected-row) product is bitwise equal to the same row of the dense one.
 //
@@ -17,16 +25,19 @@
 //   GELU      out = gelu_erf(C + b)           (storage dtype)
 //   RESIDUAL  out[row'] = resid + C + b       (fp32; row' may scatter into
 //                                              the output cache, Eq. 9)
-//   QKV       q rows, and key/value rows written straight into the per-block
+//   QKV       q rows, and keys/values written straight into the per-block
 //             cache at the row's (slot, token): the cache update of Eq. 9.
+//             Keys are stored [slot, head, token, d]; values transposed,
+//             [slot, head, d, token], the layout the attention kernel's
+//             second product reads.
 #include "common.h"
 
 namespace marcache {
 
 template <typename T> struct Mma;
 
+// One k-step = 32 bytes of K per row (two 16-byte chunks, one per lane half).
 template <> struct Mma<bf16_t> {
-  static constexpr int kBK = 64;  // elements per 128-byte LDS row
   static __device__ __forceinline__ void run(f32x16_t& acc, const u32x4_t& a, const u32x4_t& b) {
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                   __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
@@ -34,7 +45,6 @@ template <> struct Mma<bf16_t> {
 };
 
 template <> struct Mma<float> {
-  static constexpr int kBK = 32;
   static __device__ __forceinline__ void run(f32x16_t& acc, const u32x4_t& a, const u32x4_t& b) {
 #pragma unroll
     for (int j = 0; j < 4; ++j)
@@ -43,8 +53,22 @@ template <> struct Mma<float> {
   }
 };
 
+// GELU x * Phi(x) = 0.5 x (1 + erf(x / sqrt 2)), with erf from Abramowitz &
+// Stegun, Handbook of Mathematical Functions, formula 7.1.26:
+//   erf(z) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-z^2),
+//   t = 1 / (1 + p z), z >= 0, |error| <= 1.5e-7,
+// far below the bf16 rounding of the product it feeds.  With
+// q = (1 - erf(|x| / sqrt 2)) / 2:  gelu(x) = x (1 - q) for x >= 0, x q else.
 __device__ __forceinline__ float gelu_erf(float x) {
-  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752440f));
+  const float z = fabsf(x) * 0.70710678118654752440f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, z, 1.0f));
+  float poly = fmaf(1.061405429f, t, -1.453152027f);
+  poly = fmaf(poly, t, 1.421413741f);
+  poly = fmaf(poly, t, -0.284496736f);
+  poly = fmaf(poly, t, 0.254829592f);
+  poly *= t;
+  const float q = 0.5f * poly * __expf(-z * z);
+  return x >= 0.0f ? x * (1.0f - q) : x * q;
 }
 
 template <typename T>
@@ -54,62 +78,195 @@ __device__ __forceinline__ void store_elem<float>(float* p, float v) { *p = v; }
 template <>
 __device__ __forceinline__ void store_elem<bf16_t>(bf16_t* p, float v) { *p = f2bf(v); }
 
-// Epilogue for 4 consecutive rows m0..m0+3 at column n.
+typedef __attribute__((ext_vector_type(4))) int i32x4_t;
+
+// Buffer descriptor over `bytes` bytes at `base` (raw, no stride).
+__device__ __forceinline__ i32x4_t make_rsrc(const void* base, unsigned bytes) {
+  const unsigned long p = reinterpret_cast<unsigned long>(base);
+  i32x4_t r;
+  r[0] = __builtin_amdgcn_readfirstlane(static_cast<int>(p & 0xFFFFFFFFu));
+  r[1] = __builtin_amdgcn_readfirstlane(static_cast<int>(p >> 32));
+  r[2] = __builtin_amdgcn_readfirstlane(static_cast<int>(bytes));
+  r[3] = 0x00020000;
+  return r;
+}
+
+// Sixteen bytes per lane from the buffer (byte offset voff + soff) into LDS at
+// lds_addr + 16 * lane.  Issued from asm so the compiler adds no waits of its
+// own (it would drain every load before each LDS read); the main loop waits
+// with s_waitcnt vmcnt for exactly the slice it is about to read.
+// m0 is reserved by the compiler but nothing else in these kernels uses it
+// (no LDS-DMA builtins, GWS or messages), so clobbering it here is safe.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(i32x4_t rsrc, unsigned lds_addr, int voff, int soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(rsrc),
+                 "s"(__builtin_amdgcn_readfirstlane(soff))
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// physical 16-byte chunk of logical chunk c in LDS row r
+__device__ __forceinline__ int swz(int row, int c) { return c ^ ((row >> 1) & 7); }
+
+// ---------------------------------------------------------------------------
+// Epilogues.  Stores go through buffer descriptors: the row part of an
+// address is a wave-uniform SGPR offset, the column part one VGPR per tile,
+// and any element whose offset falls outside the descriptor (rows past M,
+// columns past N) is dropped by the hardware range check, so no store needs
+// a branch.  Offsets are 32-bit: the launcher keeps every output below 2 GiB.
+// ---------------------------------------------------------------------------
+constexpr int kOob = 0x7FFFFFF0;  // an offset past every descriptor
+
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+__device__ __forceinline__ rsrc_t make_out(void* base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, 0, static_cast<int>(bytes), 0x00020000);
+}
+__device__ __forceinline__ void bstore(rsrc_t r, int voff, int soff, float v, float*) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, soff, 0);
+}
+__device__ __forceinline__ void bstore(rsrc_t r, int voff, int soff, float v, bf16_t*) {
+  __builtin_amdgcn_raw_buffer_store_b16(f2bf(v), r, voff, soff, 0);
+}
+__device__ __forceinline__ float bload_f32(rsrc_t r, int voff, int soff) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+
+// Descriptors of an epilogue's outputs and inputs.
 template <typename T, int KIND>
-__device__ __forceinline__ void epilogue4(const EpiArgs& e, int M, int N, int m0, int n,
-                                          const float* v) {
-  if (n >= N) return;
-  const float bias = e.bias[n];
+struct EpiCtx {
+  rsrc_t out, aux0, aux1, aux2;
+};
+
+// Epilogue of one 32x32 MFMA tile: acc[4*g + r] is row m_tile + 8*g + rq + r,
+// column n (one per lane).
+template <typename T, int KIND>
+__device__ __forceinline__ void epilogue_tile(const EpiArgs& e, const EpiCtx<T, KIND>& c, int M, int N,
+                                              int m_tile, int rq, int n, float bias, const f32x16_t& acc) {
+  constexpr int ES = sizeof(T);
+  const bool n_ok = n < N;
   if constexpr (KIND == EPI_BIAS || KIND == EPI_GELU) {
-    T* out = static_cast<T*>(e.out);
+    const int voff = n_ok ? ((m_tile + rq) * N + n) * ES : kOob;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = m0 + i;
-      if (m < M) {
-        float x = v[i] + bias;
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float x = acc[4 * g + r] + bias;
         if constexpr (KIND == EPI_GELU) x = gelu_erf(x);
-        store_elem<T>(out + static_cast<long>(m) * N + n, x);
+        bstore(c.out, voff, (8 * g + r) * N * ES, x, static_cast<T*>(nullptr));
       }
-    }
   } else if constexpr (KIND == EPI_RESIDUAL) {
-    float* out = static_cast<float*>(e.out);
+    // aux0: resid rows [M, N]; aux1: resid_copy (or none); out: rows [M, N]
+    // or the output cache when out_idx remaps rows
+    const int nc = n_ok ? n : 0;
+    const int lin = n_ok ? ((m_tile + rq) * N + n) * 4 : kOob;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = m0 + i;
-      if (m < M) {
-        const long src = static_cast<long>(m) * N + n;
-        const float x = e.resid[src] + (v[i] + bias);
+    for (int g = 0; g < 4; ++g) {
+      float res[4];
+      int oo[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m_tile + 8 * g + rq + r;
+        res[r] = bload_f32(c.aux0, lin, (8 * g + r) * N * 4);
         if (e.out_idx) {
-          const long slot = m / e.per_slot;
-          out[(slot * e.seq + e.out_idx[m]) * N + n] = x;
-          if (e.resid_copy) e.resid_copy[src] = x;
+          const int mc = min(m, M - 1);
+          const int orow = (div_by(mc, e.slot_magic, e.slot_shift)) * e.seq + e.out_idx[mc];
+          oo[r] = (n_ok && m < M) ? (orow * N + nc) * 4 : kOob;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float x = res[r] + (acc[4 * g + r] + bias);
+        if (e.out_idx) {
+          bstore(c.out, oo[r], 0, x, static_cast<float*>(nullptr));
+          if (e.resid_copy) bstore(c.aux1, lin, (8 * g + r) * N * 4, x, static_cast<float*>(nullptr));
         } else {
-          out[src] = x;
+          bstore(c.out, lin, (8 * g + r) * N * 4, x, static_cast<float*>(nullptr));
         }
       }
     }
-  } else {  // EPI_QKV
-    const int ng = n + e.n_offset;
+  } else {  // EPI_QKV: out = q rows [M, D]; aux0 = key cache; aux1 = value cache; aux2 = value copy
+    const int nc = n_ok ? n : N - 1;
+    const int ng = nc + e.n_offset;
     const int sec = ng / e.d_model;
     const int rem = ng - sec * e.d_model;
     const int head = rem / e.d_head;
     const int d = rem - head * e.d_head;
+    if (sec == 0) {
+      const int voff = n_ok ? ((m_tile + rq) * e.d_model + rem) * ES : kOob;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = m0 + i;
-      if (m < M) {
-        const float x = v[i] + bias;
-        if (sec == 0) {
-          store_elem<T>(static_cast<T*>(e.out) + static_cast<long>(m) * e.d_model + rem, x);
-        } else {
-          const long slot = m / e.per_slot;
-          const long tok = e.idx ? static_cast<long>(e.idx[m]) : (m - slot * e.per_slot);
-          const long off = ((slot * e.n_heads + head) * e.seq + tok) * e.d_head + d;
-          if (sec == 1) {
-            store_elem<T>(static_cast<T*>(e.k_cache) + off, x);
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          bstore(c.out, voff, (8 * g + r) * e.d_model * ES, acc[4 * g + r] + bias, static_cast<T*>(nullptr));
+    } else if (sec == 1) {
+      // keys: [slot, head, token, d]
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        int off[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = m_tile + 8 * g + rq + r;
+          const int mc = min(m, M - 1);
+          const int slot = div_by(mc, e.slot_magic, e.slot_shift);
+          const int tok = e.idx ? e.idx[mc] : mc - slot * e.per_slot;
+          off[r] = (n_ok && m < M) ? (((slot * e.n_heads + head) * e.seq + tok) * e.d_head + d) * ES : kOob;
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) bstore(c.aux0, off[r], 0, acc[4 * g + r] + bias, static_cast<T*>(nullptr));
+      }
+    } else {
+      // values: the cache holds them transposed, [slot, head, d, token]; the
+      // optional copy keeps token rows, [slot, head, token, d]
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int m0 = m_tile + 8 * g + rq;
+        float x[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) x[r] = acc[4 * g + r] + bias;
+        if (!e.idx && (e.per_slot & 3) == 0) {
+          // dense rows m0..m0+3 are four consecutive tokens of one slot
+          const int slot = div_by(m0, e.slot_magic, e.slot_shift);
+          const int tok = m0 - slot * e.per_slot;
+          const int off = (n_ok && m0 < M) ? (((slot * e.n_heads + head) * e.d_head + d) * e.seq + tok) * ES : kOob;
+          if constexpr (ES == 2) {
+            const uint32_t lo = pack2bf(x[0], x[1]), hi = pack2bf(x[2], x[3]);
+            __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{lo, hi}, c.aux1, off, 0, 0);
           } else {
-            store_elem<T>(static_cast<T*>(e.v_cache) + off, x);
-            if (e.v_copy) store_elem<T>(static_cast<T*>(e.v_copy) + off, x);
+            __builtin_amdgcn_raw_buffer_store_b128(
+                u32x4_t{__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]), __float_as_uint(x[3])},
+                c.aux1, off, 0, 0);
+          }
+          if (e.v_copy) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int offc = (n_ok && m0 < M) ? (((slot * e.n_heads + head) * e.seq + tok + r) * e.d_head + d) * ES : kOob;
+              bstore(c.aux2, offc, 0, x[r], static_cast<T*>(nullptr));
+            }
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int m = m0 + r;
+            const int mc = min(m, M - 1);
+            const int slot = div_by(mc, e.slot_magic, e.slot_shift);
+            const int tok = e.idx ? e.idx[mc] : mc - slot * e.per_slot;
+            const bool ok = n_ok && m < M;
+            bstore(c.aux1, ok ? (((slot * e.n_heads + head) * e.d_head + d) * e.seq + tok) * ES : kOob, 0, x[r],
+                   static_cast<T*>(nullptr));
+            if (e.v_copy)
+              bstore(c.aux2, ok ? (((slot * e.n_heads + head) * e.seq + tok) * e.d_head + d) * ES : kOob, 0, x[r],
+                     static_cast<T*>(nullptr));
           }
         }
       }
@@ -117,68 +274,95 @@ __device__ __forceinline__ void epilogue4(const EpiArgs& e, int M, int N, int m0
   }
 }
 
-template <typename T, int BM, int BN, int KIND>
-__global__ __launch_bounds__(256) void gemm_kernel(const T* __restrict__ A,
-                                                   const T* __restrict__ W, int M, int N, int K,
-                                                   EpiArgs e) {
-  constexpr int BK = Mma<T>::kBK;
-  constexpr int PER = Elem<T>::kPer16B;       // elements per 16-byte vector
-  constexpr int VROW = BK / PER;              // 16-byte vectors per LDS row (8)
-  constexpr int LROW = BK + PER;              // padded LDS row (elements): 144 bytes
-  constexpr int WM = BM / 2, WN = BN / 2;     // wave tile
-  constexpr int TM = WM / 32, TN = WN / 32;   // MFMA tiles per wave
-  constexpr int A_LOADS = BM * VROW / 256;    // 16-byte loads per thread per slice
-  constexpr int B_LOADS = BN * VROW / 256;
+template <typename T, int KIND>
+__device__ __forceinline__ EpiCtx<T, KIND> make_epi(const EpiArgs& e, int M, int N) {
+  constexpr unsigned ES = sizeof(T);
+  EpiCtx<T, KIND> c;
+  if constexpr (KIND == EPI_BIAS || KIND == EPI_GELU) {
+    c.out = make_out(e.out, static_cast<unsigned>(M) * N * ES);
+    c.aux0 = c.aux1 = c.aux2 = c.out;
+  } else if constexpr (KIND == EPI_RESIDUAL) {
+    const unsigned rows = e.out_idx ? static_cast<unsigned>((M + e.per_slot - 1) / e.per_slot) * e.seq
+                                    : static_cast<unsigned>(M);
+    c.out = make_out(e.out, rows * N * 4u);
+    c.aux0 = make_out(const_cast<float*>(e.resid), static_cast<unsigned>(M) * N * 4u);
+    c.aux1 = make_out(e.resid_copy, e.resid_copy ? static_cast<unsigned>(M) * N * 4u : 0u);
+    c.aux2 = c.aux1;
+  } else {
+    const unsigned slots = static_cast<unsigned>((M + e.per_slot - 1) / e.per_slot);
+    const unsigned cache = slots * e.n_heads * e.seq * e.d_head * ES;
+    c.out = make_out(e.out, e.out ? static_cast<unsigned>(M) * e.d_model * ES : 0u);
+    c.aux0 = make_out(e.k_cache, e.k_cache ? cache : 0u);
+    c.aux1 = make_out(e.v_cache, e.v_cache ? cache : 0u);
+    c.aux2 = make_out(e.v_copy, e.v_copy ? cache : 0u);
+  }
+  return c;
+}
 
-  extern __shared__ __align__(16) unsigned char smem[];
-  T* As = reinterpret_cast<T*>(smem);                    // [2][BM][LROW]
-  T* Bs = As + 2 * BM * LROW;                            // [2][BN][LROW]
+// Tile BM x BN, WAVES_M x WAVES_N waves, each wave (BM / WAVES_M) x
+// (BN / WAVES_N); STAGES LDS buffers of (BM + BN) rows x 128 bytes.
+template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int KIND>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* __restrict__ A,
+                                                                    const T* __restrict__ W, int M,
+                                                                    int N, int K, EpiArgs e) {
+  constexpr int NW = WAVES_M * WAVES_N;
+  constexpr int ROWB = 128;                    // bytes of K per LDS row and slice
+  constexpr int STAGE_BYTES = (BM + BN) * ROWB;
+  constexpr int A_INSTR = BM / 8 / NW;         // 8 rows (1 KiB) per wave-wide load
+  constexpr int B_INSTR = BN / 8 / NW;
+  constexpr int LOADS = A_INSTR + B_INSTR;     // loads per wave per slice
+  constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int KSTEPS = ROWB / 32;            // MFMA k-steps per slice
+  static_assert(A_INSTR * 8 * NW == BM && B_INSTR * 8 * NW == BN, "tile/waves");
+  static_assert(STAGES >= 2 && STAGES <= 4, "stages");
+
+  __shared__ __align__(1024) unsigned char s0[STAGE_BYTES];
+  __shared__ __align__(1024) unsigned char s1[STAGE_BYTES];
+  __shared__ __align__(1024) unsigned char s2[STAGES > 2 ? STAGE_BYTES : 16];
+  __shared__ __align__(1024) unsigned char s3[STAGES > 3 ? STAGE_BYTES : 16];
+  unsigned char* const stage[4] = {s0, s1, s2, s3};
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WAVES_N, wn = wave - (wave / WAVES_N) * WAVES_N;
   const int tiles_n = (N + BN - 1) / BN;
   const int tile_m = blockIdx.x / tiles_n;
   const int tile_n = blockIdx.x - tile_m * tiles_n;
   const int m_base = tile_m * BM;
   const int n_base = tile_n * BN;
+  const int col = lane & 31;
+  const int rq = (lane >> 5) * 4;
 
-  u32x4_t ra[A_LOADS], rb[B_LOADS];
-  const u32x4_t zero = {0u, 0u, 0u, 0u};
+  // epilogue bias of this lane's columns, fetched before the main loop
+  float bias[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) bias[j] = e.bias[min(n_base + wn * WN + j * 32 + col, N - 1)];
 
-  auto load_slice = [&](int k0) {
+  const int Kb = K * static_cast<int>(sizeof(T));
+  const i32x4_t ra = make_rsrc(A + static_cast<long>(m_base) * K,
+                               static_cast<unsigned>(min(BM, M - m_base)) * Kb);
+  const i32x4_t rb = make_rsrc(W + static_cast<long>(n_base) * K,
+                               static_cast<unsigned>(min(BN, N - n_base)) * Kb);
+  const int KT = Kb / ROWB;
+  // lane's place in a wave-wide load: row r_in of 8, physical chunk pc
+  const int r_in = lane >> 3, pc = lane & 7;
+  auto issue = [&](unsigned char* st, int kt) {
+    const int kb = kt < KT ? kt * ROWB : 0;  // past the end: a harmless reload of slice 0
 #pragma unroll
-    for (int i = 0; i < A_LOADS; ++i) {
-      const int v = tid + 256 * i;
-      const int r = v / VROW, c = v - r * VROW;
-      const int m = m_base + r;
-      ra[i] = (m < M) ? *reinterpret_cast<const u32x4_t*>(A + static_cast<long>(m) * K + k0 + c * PER)
-                      : zero;
+    for (int i = 0; i < A_INSTR; ++i) {
+      const int grp = wave * A_INSTR + i;
+      const int row = grp * 8 + r_in;
+      dma16(ra, static_cast<unsigned>(reinterpret_cast<uintptr_t>(st + grp * 1024)),
+            row * Kb + swz(row, pc) * 16, kb);
     }
 #pragma unroll
-    for (int i = 0; i < B_LOADS; ++i) {
-      const int v = tid + 256 * i;
-      const int r = v / VROW, c = v - r * VROW;
-      const int n = n_base + r;
-      rb[i] = (n < N) ? *reinterpret_cast<const u32x4_t*>(W + static_cast<long>(n) * K + k0 + c * PER)
-                      : zero;
-    }
-  };
-  auto store_slice = [&](int buf) {
-    T* as = As + buf * BM * LROW;
-    T* bs = Bs + buf * BN * LROW;
-#pragma unroll
-    for (int i = 0; i < A_LOADS; ++i) {
-      const int v = tid + 256 * i;
-      const int r = v / VROW, c = v - r * VROW;
-      *reinterpret_cast<u32x4_t*>(as + r * LROW + c * PER) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < B_LOADS; ++i) {
-      const int v = tid + 256 * i;
-      const int r = v / VROW, c = v - r * VROW;
-      *reinterpret_cast<u32x4_t*>(bs + r * LROW + c * PER) = rb[i];
+    for (int i = 0; i < B_INSTR; ++i) {
+      const int grp = wave * B_INSTR + i;
+      const int row = grp * 8 + r_in;
+      dma16(rb, static_cast<unsigned>(reinterpret_cast<uintptr_t>(st + BM * ROWB + grp * 1024)),
+            row * Kb + swz(row, pc) * 16, kb);
     }
   };
 
@@ -190,78 +374,175 @@ __global__ __launch_bounds__(256) void gemm_kernel(const T* __restrict__ A,
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int KT = K / BK;
-  load_slice(0);
-  store_slice(0);
-  __syncthreads();
-
-  const int frag_row = lane & 31;
-  const int frag_k = (lane >> 5) * PER;  // element offset of this lane's 16 bytes
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) load_slice((kt + 1) * BK);
-    const T* as = As + buf * BM * LROW + (wm * WM + frag_row) * LROW + frag_k;
-    const T* bs = Bs + buf * BN * LROW + (wn * WN + frag_row) * LROW + frag_k;
+  const int frow = lane & 31, fch = lane >> 5;
+  auto frag_a = [&](const unsigned char* st, int i, int kk) {
+    const int row = wm * WM + i * 32 + frow;
+    return *reinterpret_cast<const u32x4_t*>(st + row * ROWB + swz(row, 2 * kk + fch) * 16);
+  };
+  auto frag_b = [&](const unsigned char* st, int j, int kk) {
+    const int row = wn * WN + j * 32 + frow;
+    return *reinterpret_cast<const u32x4_t*>(st + BM * ROWB + row * ROWB + swz(row, 2 * kk + fch) * 16);
+  };
+  // fragments of k-step kk+1 are read while k-step kk multiplies
+  auto compute = [&](const unsigned char* st) {
+    u32x4_t fa[2][TM], fb[2][TN];
 #pragma unroll
-    for (int kk = 0; kk < BK / (2 * PER); ++kk) {
-      u32x4_t fa[TM], fb[TN];
+    for (int i = 0; i < TM; ++i) fa[0][i] = frag_a(st, i, 0);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) fb[0][j] = frag_b(st, j, 0);
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; ++kk) {
+      const int cur = kk & 1;
+      if (kk + 1 < KSTEPS) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) fa[cur ^ 1][i] = frag_a(st, i, kk + 1);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) fb[cur ^ 1][j] = frag_b(st, j, kk + 1);
+      }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
-        fa[i] = *reinterpret_cast<const u32x4_t*>(as + i * 32 * LROW + kk * 2 * PER);
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-        fb[j] = *reinterpret_cast<const u32x4_t*>(bs + j * 32 * LROW + kk * 2 * PER);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) Mma<T>::run(acc[i][j], fa[i], fb[j]);
+        for (int j = 0; j < TN; ++j) Mma<T>::run(acc[i][j], fa[cur][i], fb[cur][j]);
     }
-    if (kt + 1 < KT) store_slice(buf ^ 1);
-    __syncthreads();
-  }
+  };
 
-  // acc[i][j][4*g + r] holds row 8*g + 4*(lane/32) + r, column lane%32 of
-  // the 32x32 tile (i, j).
-  const int col = lane & 31;
-  const int rq = (lane >> 5) * 4;
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s) issue(stage[s], s);
+  for (int kt0 = 0; kt0 < KT; kt0 += STAGES) {
+#pragma unroll
+    for (int u = 0; u < STAGES; ++u) {
+      const int kt = kt0 + u;
+      if (kt < KT) {
+        // every wave's slice kt has landed once each wave has waited for
+        // its own loads (one load group per slice is issued per iteration)
+        wait_vm<LOADS * (STAGES - 2)>();
+        __builtin_amdgcn_s_barrier();
+        // the buffer of slice kt-1 is free: every wave passed the barrier
+        // after reading it
+        issue(stage[(u + STAGES - 1) % STAGES], kt + STAGES - 1);
+        compute(stage[u]);
+      }
+    }
+  }
+  wait_vm<0>();  // no load may still target this workgroup's LDS
+
+  const EpiCtx<T, KIND> ec = make_epi<T, KIND>(e, M, N);
+  if constexpr (KIND == EPI_QKV && sizeof(T) == 2) {
+    // Dense value columns go to the transposed cache through LDS, so that
+    // each lane stores 16 bytes of consecutive tokens of one dimension.  A
+    // wave stages its WN x WM tile as rows of dimensions (WM tokens each),
+    // 16-byte chunks XOR-swizzled by the row so that writes and reads spread
+    // over the banks; a wave's region never straddles two ring buffers.
+    constexpr int ROWB_V = WM * 2;                      // bytes per staged row
+    constexpr int NCH = ROWB_V / 16;                    // chunks per row
+    constexpr int REGION = WN * ROWB_V;
+    constexpr int PER_BUF = STAGE_BYTES / REGION;       // wave regions per ring buffer
+    static_assert(PER_BUF >= 1 && (NW + PER_BUF - 1) / PER_BUF <= STAGES, "value staging fits the LDS ring");
+    static_assert((NCH & (NCH - 1)) == 0, "power-of-two chunks per row");
+    if (!e.idx && (e.per_slot & 7) == 0) {
+      __syncthreads();  // every wave is done with the LDS ring
+      const int n_wave = n_base + wn * WN;
+      const bool wave_v = n_wave < N && (n_wave + e.n_offset) / e.d_model == 2;
+      if (wave_v) {
+        const int bufi = wave / PER_BUF;
+        unsigned char* reg = (bufi == 0 ? s0 : bufi == 1 ? s1 : bufi == 2 ? s2 : s3) + (wave % PER_BUF) * REGION;
+        auto at = [&](int row, int byte) {  // byte offset within the row
+          return reg + row * ROWB_V + ((((byte >> 4) ^ row) & (NCH - 1)) << 4) + (byte & 15);
+        };
+        // acc[i][j][4 g + r]: token row wm*WM + 32 i + 8 g + rq + r, d column 32 j + col
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const float bj = bias[j];
+              const u32x2_t w = {pack2bf(acc[i][j][4 * g] + bj, acc[i][j][4 * g + 1] + bj),
+                                 pack2bf(acc[i][j][4 * g + 2] + bj, acc[i][j][4 * g + 3] + bj)};
+              *reinterpret_cast<u32x2_t*>(at(32 * j + col, (32 * i + 8 * g + rq) * 2)) = w;
+            }
+        // read back 16-byte runs of 8 tokens: WN rows x WM / 8 chunks
+        const int rem0 = (n_wave + e.n_offset) - 2 * e.d_model;
+        constexpr int CHUNKS = WN * (WM / 8);
+#pragma unroll
+        for (int it = 0; it < CHUNKS / 64; ++it) {
+          const int v = lane + 64 * it;
+          const int dl = v / (WM / 8), c = v - dl * (WM / 8);
+          const u32x4_t val = *reinterpret_cast<const u32x4_t*>(at(dl, c * 16));
+          const int m = m_base + wm * WM + 8 * c;
+          const int rem = rem0 + dl;
+          const int head = rem / e.d_head, d = rem - head * e.d_head;
+          const int slot = div_by(m, e.slot_magic, e.slot_shift), tok = m - slot * e.per_slot;
+          const int off = (m < M && n_wave + dl < N)
+                              ? (((slot * e.n_heads + head) * e.d_head + d) * e.seq + tok) * 2 : kOob;
+          __builtin_amdgcn_raw_buffer_store_b128(val, ec.aux1, off, 0, 0);
+        }
+        if (e.v_copy) {  // token rows as well (the scoring block)
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+              for (int g = 0; g < 4; ++g)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                  const int m = m_base + wm * WM + 32 * i + 8 * g + rq + r;
+                  const int rem = rem0 + 32 * j + col;
+                  const int head = rem / e.d_head, d = rem - head * e.d_head;
+                  const int slot = div_by(m, e.slot_magic, e.slot_shift), tok = m - slot * e.per_slot;
+                  const int off = (m < M && n_wave + 32 * j + col < N)
+                                      ? (((slot * e.n_heads + head) * e.seq + tok) * e.d_head + d) * 2 : kOob;
+                  bstore(ec.aux2, off, 0, acc[i][j][4 * g + r] + bias[j], static_cast<T*>(nullptr));
+                }
+        }
+        return;
+      }
+    }
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        float v4[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
-                       acc[i][j][4 * g + 3]};
-        const int m0 = m_base + wm * WM + i * 32 + 8 * g + rq;
-        const int n = n_base + wn * WN + j * 32 + col;
-        epilogue4<T, KIND>(e, M, N, m0, n, v4);
-      }
+    for (int j = 0; j < TN; ++j) {
+      epilogue_tile<T, KIND>(e, ec, M, N, m_base + wm * WM + i * 32, rq, n_base + wn * WN + j * 32 + col,
+                             bias[j], acc[i][j]);
+      __builtin_amdgcn_sched_barrier(0);  // keep each tile's loads with its stores
+    }
 }
 
-template <typename T, int BM, int BN, int KIND>
+template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int KIND>
 static hipError_t gemm_launch(const void* A, const void* W, int M, int N, int K,
                               const EpiArgs& e, hipStream_t st) {
-  constexpr int BK = Mma<T>::kBK;
-  constexpr int LROW = BK + Elem<T>::kPer16B;
-  const size_t lds = static_cast<size_t>(2) * (BM + BN) * LROW * sizeof(T);
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t err = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&gemm_kernel<T, BM, BN, KIND>),
-        hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-    if (err != hipSuccess) return err;
-    attr_set = true;
-  }
   const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, KIND>), dim3(tiles), dim3(256), lds, st,
-                     static_cast<const T*>(A), static_cast<const T*>(W), M, N, K, e);
+  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WAVES_M, WAVES_N, STAGES, KIND>), dim3(tiles),
+                     dim3(64 * WAVES_M * WAVES_N), 0, st, static_cast<const T*>(A),
+                     static_cast<const T*>(W), M, N, K, e);
   return hipGetLastError();
 }
+
+// Tile choice.  Every configuration uses the same MFMA and visits k in the
+// same order, so the choice never changes a result bit.
+int g_gemm_variant = -1;  // test hook: force a variant (-1 = by shape)
 
 template <typename T, int KIND>
 static hipError_t gemm_pick(const void* A, const void* W, int M, int N, int K, const EpiArgs& e,
                             hipStream_t st) {
-  return gemm_launch<T, 128, 128, KIND>(A, W, M, N, K, e, st);
+  int v = g_gemm_variant;
+  if (v < 0) {
+    // (measured on MI355X) 128 x 128 tiles with a 3-deep prefetch when each
+    // CU gets at most one of them; otherwise 256 x 256 tiles once there are
+    // at least half as many as CUs, and 128 x 128 tiles with two workgroups
+    // per CU below that
+    const long big = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
+    const long small = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
+    v = small <= 256 ? 1 : (big >= 128 ? 0 : 4);
+  }
+  switch (v) {
+    case 0: return gemm_launch<T, 256, 256, 2, 4, 2, KIND>(A, W, M, N, K, e, st);
+    case 1: return gemm_launch<T, 128, 128, 2, 2, 3, KIND>(A, W, M, N, K, e, st);
+    case 2: return gemm_launch<T, 256, 128, 2, 2, 3, KIND>(A, W, M, N, K, e, st);
+    case 3: return gemm_launch<T, 128, 256, 2, 2, 3, KIND>(A, W, M, N, K, e, st);
+    default: return gemm_launch<T, 128, 128, 2, 2, 2, KIND>(A, W, M, N, K, e, st);
+  }
 }
 
 template <typename T>
@@ -276,9 +557,30 @@ static hipError_t gemm_kind(const void* A, const void* W, int M, int N, int K, c
   }
 }
 
+void set_gemm_variant(int v) { g_gemm_variant = v; }
+
 hipError_t launch_gemm(int dtype, const void* A, const void* W, int M, int N, int K,
-                       const EpiArgs& e, hipStream_t st) {
+                       const EpiArgs& e_in, hipStream_t st) {
   if (M == 0 || N == 0) return hipSuccess;
+  EpiArgs e = e_in;
+  if (e.kind == EPI_QKV || (e.kind == EPI_RESIDUAL && e.out_idx)) {
+    if (e.per_slot < 1) return hipErrorInvalidValue;
+    const Divisor dv = make_divisor(static_cast<uint32_t>(e.per_slot));
+    e.slot_magic = dv.magic;
+    e.slot_shift = dv.shift;
+  }
+  // 32-bit buffer offsets: a tile's operand rows and every output must span
+  // less than 2 GiB
+  const size_t es = dtype == DT_BF16 ? 2 : 4;
+  const size_t lim = 1ull << 31;
+  if (static_cast<size_t>(256) * K * es >= lim || (K * es) % 128) return hipErrorInvalidValue;
+  if (static_cast<size_t>(M) * N * 4 >= lim) return hipErrorInvalidValue;
+  if (e.kind == EPI_RESIDUAL && e.out_idx &&
+      static_cast<size_t>((M + e.per_slot - 1) / e.per_slot) * e.seq * N * 4 >= lim)
+    return hipErrorInvalidValue;
+  if (e.kind == EPI_QKV && static_cast<size_t>((M + e.per_slot - 1) / e.per_slot) * e.n_heads * e.seq *
+                                   e.d_head * es >= lim)
+    return hipErrorInvalidValue;
   if (dtype == DT_BF16) return gemm_kind<bf16_t>(A, W, M, N, K, e, st);
   return gemm_kind<float>(A, W, M, N, K, e, st);
 }
