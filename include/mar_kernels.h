@@ -39,7 +39,7 @@ mar_status mar_k_layernorm(int32_t dtype, const void* src, int32_t src_f32, cons
 
 /* out[m, n] = act(a w^T + bias) in dtype; a [m, k], w [n, k] (nn.Linear
  * layout), bias [n] fp32; act = exact-erf GELU when `act` != 0 (the block's
- * first MLP product), identity otherwise.  k % 64 == 0. */
+ * first MLP product), identity otherwise.  k % 64 == 0, n % 8 == 0. */
 mar_status mar_k_linear(int32_t dtype, int32_t act, const void* a, const void* w, const float* bias,
                         int32_t m, int32_t n, int32_t k, void* out, void* stream);
 
@@ -47,7 +47,8 @@ mar_status mar_k_linear(int32_t dtype, int32_t act, const void* a, const void* w
  *   x[m, n] = resid[m, n] + (a w^T)[m, n] + bias[n]      fp32
  * written to out[m, n] (out may equal resid), or, when out_idx is given, to
  * out[(m / per_slot) * seq + out_idx[m], n] (the scatter of the fresh rows
- * into the output cache, Eq. 9) with resid_copy[m, n] = x (nullable). */
+ * into the output cache, Eq. 9) with resid_copy[m, n] = x (nullable).
+ * k % 64 == 0, n % 8 == 0. */
 mar_status mar_k_linear_residual(int32_t dtype, const void* a, const void* w, const float* bias,
                                  int32_t m, int32_t n, int32_t k, const float* resid, float* out,
                                  const int32_t* out_idx, int32_t per_slot, int32_t seq,
@@ -62,7 +63,8 @@ mar_status mar_k_linear_residual(int32_t dtype, const void* a, const void* w, co
  *   value columns  -> v_cache[slot, head, :, tok]  ([slots, H, dh, seq],
  *                     transposed; nullable) and v_copy[slot, head, tok, :]
  *                     ([slots, H, seq, dh]; nullable); one of them required
- * slot/tok from the row mapping.  d_model % 64 == 0. */
+ * slot/tok from the row mapping.  d_model % 64 == 0, d_head % 16 == 0,
+ * n_offset % 32 == 0, n_cols % 8 == 0. */
 mar_status mar_k_qkv(int32_t dtype, const void* a, const void* w, const float* bias, int32_t m,
                      int32_t n_cols, int32_t n_offset, int32_t d_model, int32_t n_heads, int32_t seq,
                      int32_t per_slot, const int32_t* idx, void* q_out, void* k_cache, void* v_cache,

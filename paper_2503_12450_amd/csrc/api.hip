@@ -689,8 +689,9 @@ mar_status mar_k_linear(int32_t dtype, int32_t act, const void* a, const void* w
   g_err.clear();
   if (check_dtype(dtype) != MAR_OK) return MAR_E_ARG;
   if (!a || !w || !bias || !out) return fail(MAR_E_ARG, "NULL pointer");
-  if (m < 0 || n < 1 || k < 64 || k % 64) return fail(MAR_E_SHAPE, "k must be a positive multiple of 64");
-  if (!aligned16(a) || !aligned16(w)) return fail(MAR_E_ARG, "operands must be 16-byte aligned");
+  if (m < 0 || k < 64 || k % 64) return fail(MAR_E_SHAPE, "k must be a positive multiple of 64");
+  if (n < 8 || n % 8) return fail(MAR_E_SHAPE, "n must be a positive multiple of 8");
+  if (!aligned16(a) || !aligned16(w) || !aligned16(out)) return fail(MAR_E_ARG, "operands must be 16-byte aligned");
   EpiArgs e{};
   e.kind = act ? EPI_GELU : EPI_BIAS;
   e.bias = bias;
@@ -706,9 +707,12 @@ mar_status mar_k_linear_residual(int32_t dtype, const void* a, const void* w, co
   g_err.clear();
   if (check_dtype(dtype) != MAR_OK) return MAR_E_ARG;
   if (!a || !w || !bias || !resid || !out) return fail(MAR_E_ARG, "NULL pointer");
-  if (m < 0 || n < 1 || k < 64 || k % 64) return fail(MAR_E_SHAPE, "k must be a positive multiple of 64");
+  if (m < 0 || k < 64 || k % 64) return fail(MAR_E_SHAPE, "k must be a positive multiple of 64");
+  if (n < 8 || n % 8) return fail(MAR_E_SHAPE, "n must be a positive multiple of 8");
   if (out_idx && (per_slot < 1 || seq < 1)) return fail(MAR_E_SHAPE, "bad row mapping");
-  if (!aligned16(a) || !aligned16(w)) return fail(MAR_E_ARG, "operands must be 16-byte aligned");
+  if (!aligned16(a) || !aligned16(w) || !aligned16(resid) || !aligned16(out) ||
+      (resid_copy && !aligned16(resid_copy)))
+    return fail(MAR_E_ARG, "operands must be 16-byte aligned");
   EpiArgs e{};
   e.kind = EPI_RESIDUAL;
   e.bias = bias;
@@ -729,14 +733,18 @@ mar_status mar_k_qkv(int32_t dtype, const void* a, const void* w, const float* b
   g_err.clear();
   if (check_dtype(dtype) != MAR_OK) return MAR_E_ARG;
   if (!a || !w || !bias) return fail(MAR_E_ARG, "NULL pointer");
-  if (n_heads < 1 || d_model % 64 || d_model % n_heads) return fail(MAR_E_SHAPE, "bad d_model/n_heads");
-  if (n_offset < 0 || n_cols < 1 || n_offset + n_cols > 3 * d_model) return fail(MAR_E_SHAPE, "bad columns");
+  if (n_heads < 1 || d_model % 64 || d_model % n_heads || (d_model / n_heads) % 16)
+    return fail(MAR_E_SHAPE, "bad d_model/n_heads");
+  if (n_offset < 0 || n_offset % 32 || n_cols < 8 || n_cols % 8 || n_offset + n_cols > 3 * d_model)
+    return fail(MAR_E_SHAPE, "bad columns");
   if (per_slot < 1 || seq < 1 || (!idx && per_slot != seq)) return fail(MAR_E_SHAPE, "bad row mapping");
   const bool has_q = n_offset < d_model, has_k = n_offset < 2 * d_model && n_offset + n_cols > d_model,
              has_v = n_offset + n_cols > 2 * d_model;
   if ((has_q && !q_out) || (has_k && !k_cache) || (has_v && !v_cache && !v_copy))
     return fail(MAR_E_ARG, "missing output for the requested columns");
-  if (!aligned16(a) || !aligned16(w)) return fail(MAR_E_ARG, "operands must be 16-byte aligned");
+  if (!aligned16(a) || !aligned16(w) || !aligned16(q_out) || !aligned16(k_cache) || !aligned16(v_cache) ||
+      !aligned16(v_copy))
+    return fail(MAR_E_ARG, "operands must be 16-byte aligned");
   EpiArgs e{};
   e.kind = EPI_QKV;
   e.bias = bias;

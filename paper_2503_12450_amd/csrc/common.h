@@ -134,6 +134,9 @@ struct EpiArgs {
   // m / per_slot = umulhi(m, slot_magic) >> slot_shift (set by launch_gemm)
   uint32_t slot_magic;
   int slot_shift;
+  // QKV: r / d_head = umulhi(r, head_magic) >> head_shift (set by launch_gemm)
+  uint32_t head_magic;
+  int head_shift;
   const int32_t* idx;
   void* k_cache;
   void* v_cache;

@@ -16,7 +16,8 @@
 // Math: 32x32 MFMA tiles per wave,
 //   bf16: v_mfma_f32_32x32x16_bf16 (one per 16 k)
 //   fp32: v_mfma_f32_32x32x2_f32   (four per 8 k)
-// with fp32 accumulation.  Every output element sums its k in the same order
+// with fp32 accumulation; each tile is formed transposed (weights as the
+// first operand) so that a lane ends up holding a run of one row.  Every output element sums its k in the same order
 // whatever the tile shape, M, or the row's position, so a row of a compact
 // (selected-row) product is bitwise equal to the same row of the dense one.
 //
@@ -30,6 +31,8 @@
 //             Keys are stored [slot, head, token, d]; values transposed,
 //             [slot, head, d, token], the layout the attention kernel's
 //             second product reads.
+#include <type_traits>
+
 #include "common.h"
 
 namespace marcache {
@@ -70,13 +73,6 @@ __device__ __forceinline__ float gelu_erf(float x) {
   const float q = 0.5f * poly * __expf(-z * z);
   return x >= 0.0f ? x * (1.0f - q) : x * q;
 }
-
-template <typename T>
-__device__ __forceinline__ void store_elem(T* p, float v);
-template <>
-__device__ __forceinline__ void store_elem<float>(float* p, float v) { *p = v; }
-template <>
-__device__ __forceinline__ void store_elem<bf16_t>(bf16_t* p, float v) { *p = f2bf(v); }
 
 typedef __attribute__((ext_vector_type(4))) int i32x4_t;
 
@@ -119,11 +115,20 @@ __device__ __forceinline__ void wait_vm() {
 __device__ __forceinline__ int swz(int row, int c) { return c ^ ((row >> 1) & 7); }
 
 // ---------------------------------------------------------------------------
-// Epilogues.  Stores go through buffer descriptors: the row part of an
-// address is a wave-uniform SGPR offset, the column part one VGPR per tile,
-// and any element whose offset falls outside the descriptor (rows past M,
-// columns past N) is dropped by the hardware range check, so no store needs
-// a branch.  Offsets are 32-bit: the launcher keeps every output below 2 GiB.
+// Epilogues.  The MFMA forms C^T = W A^T (weight fragment as its first
+// operand), so that acc[4 g + r] of a lane's 32 x 32 tile is output row
+// m_tile + lane % 32 and column n_tile + 8 g + 4 (lane / 32) + r: each lane
+// owns one row and four consecutive columns per group g.
+//
+// A wave finishes its tile one 32-row strip at a time: the strip's values
+// (bias added, activation applied, in the output type) are written to a
+// private LDS region as row-major rows, then read back as 16-byte chunks so
+// that eight consecutive lanes store one whole 128-byte line.  Stores go
+// through buffer descriptors; a chunk whose offset falls outside the
+// descriptor (rows past M, columns past N, absent outputs of size 0) is
+// dropped by the hardware range check, so no store needs a branch.  Offsets
+// are 32-bit: the launcher keeps every output below 2 GiB.  N is a multiple
+// of 8, so a chunk is wholly inside N or wholly outside.
 // ---------------------------------------------------------------------------
 constexpr int kOob = 0x7FFFFFF0;  // an offset past every descriptor
 
@@ -132,14 +137,24 @@ typedef __amdgpu_buffer_rsrc_t rsrc_t;
 __device__ __forceinline__ rsrc_t make_out(void* base, unsigned bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(base, 0, static_cast<int>(bytes), 0x00020000);
 }
-__device__ __forceinline__ void bstore(rsrc_t r, int voff, int soff, float v, float*) {
-  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, soff, 0);
+__device__ __forceinline__ void bstore16(rsrc_t r, int voff, const u32x4_t& v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, 0, 0);
 }
-__device__ __forceinline__ void bstore(rsrc_t r, int voff, int soff, float v, bf16_t*) {
-  __builtin_amdgcn_raw_buffer_store_b16(f2bf(v), r, voff, soff, 0);
+__device__ __forceinline__ u32x4_t bload16(rsrc_t r, int voff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0);
 }
-__device__ __forceinline__ float bload_f32(rsrc_t r, int voff, int soff) {
-  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+__device__ __forceinline__ void bstore1(rsrc_t r, int voff, float x, float*) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, voff, 0, 0);
+}
+__device__ __forceinline__ void bstore1(rsrc_t r, int voff, float x, bf16_t*) {
+  __builtin_amdgcn_raw_buffer_store_b16(f2bf(x), r, voff, 0, 0);
+}
+// four consecutive output values into LDS
+__device__ __forceinline__ void lds_put4(unsigned char* p, const float* x, float*) {
+  *reinterpret_cast<f32x4_t*>(p) = f32x4_t{x[0], x[1], x[2], x[3]};
+}
+__device__ __forceinline__ void lds_put4(unsigned char* p, const float* x, bf16_t*) {
+  *reinterpret_cast<u32x2_t*>(p) = u32x2_t{pack2bf(x[0], x[1]), pack2bf(x[2], x[3])};
 }
 
 // Descriptors of an epilogue's outputs and inputs.
@@ -147,132 +162,6 @@ template <typename T, int KIND>
 struct EpiCtx {
   rsrc_t out, aux0, aux1, aux2;
 };
-
-// Epilogue of one 32x32 MFMA tile: acc[4*g + r] is row m_tile + 8*g + rq + r,
-// column n (one per lane).
-template <typename T, int KIND>
-__device__ __forceinline__ void epilogue_tile(const EpiArgs& e, const EpiCtx<T, KIND>& c, int M, int N,
-                                              int m_tile, int rq, int n, float bias, const f32x16_t& acc) {
-  constexpr int ES = sizeof(T);
-  const bool n_ok = n < N;
-  if constexpr (KIND == EPI_BIAS || KIND == EPI_GELU) {
-    const int voff = n_ok ? ((m_tile + rq) * N + n) * ES : kOob;
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float x = acc[4 * g + r] + bias;
-        if constexpr (KIND == EPI_GELU) x = gelu_erf(x);
-        bstore(c.out, voff, (8 * g + r) * N * ES, x, static_cast<T*>(nullptr));
-      }
-  } else if constexpr (KIND == EPI_RESIDUAL) {
-    // aux0: resid rows [M, N]; aux1: resid_copy (or none); out: rows [M, N]
-    // or the output cache when out_idx remaps rows
-    const int nc = n_ok ? n : 0;
-    const int lin = n_ok ? ((m_tile + rq) * N + n) * 4 : kOob;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      float res[4];
-      int oo[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m_tile + 8 * g + rq + r;
-        res[r] = bload_f32(c.aux0, lin, (8 * g + r) * N * 4);
-        if (e.out_idx) {
-          const int mc = min(m, M - 1);
-          const int orow = (div_by(mc, e.slot_magic, e.slot_shift)) * e.seq + e.out_idx[mc];
-          oo[r] = (n_ok && m < M) ? (orow * N + nc) * 4 : kOob;
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float x = res[r] + (acc[4 * g + r] + bias);
-        if (e.out_idx) {
-          bstore(c.out, oo[r], 0, x, static_cast<float*>(nullptr));
-          if (e.resid_copy) bstore(c.aux1, lin, (8 * g + r) * N * 4, x, static_cast<float*>(nullptr));
-        } else {
-          bstore(c.out, lin, (8 * g + r) * N * 4, x, static_cast<float*>(nullptr));
-        }
-      }
-    }
-  } else {  // EPI_QKV: out = q rows [M, D]; aux0 = key cache; aux1 = value cache; aux2 = value copy
-    const int nc = n_ok ? n : N - 1;
-    const int ng = nc + e.n_offset;
-    const int sec = ng / e.d_model;
-    const int rem = ng - sec * e.d_model;
-    const int head = rem / e.d_head;
-    const int d = rem - head * e.d_head;
-    if (sec == 0) {
-      const int voff = n_ok ? ((m_tile + rq) * e.d_model + rem) * ES : kOob;
-#pragma unroll
-      for (int g = 0; g < 4; ++g)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          bstore(c.out, voff, (8 * g + r) * e.d_model * ES, acc[4 * g + r] + bias, static_cast<T*>(nullptr));
-    } else if (sec == 1) {
-      // keys: [slot, head, token, d]
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        int off[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = m_tile + 8 * g + rq + r;
-          const int mc = min(m, M - 1);
-          const int slot = div_by(mc, e.slot_magic, e.slot_shift);
-          const int tok = e.idx ? e.idx[mc] : mc - slot * e.per_slot;
-          off[r] = (n_ok && m < M) ? (((slot * e.n_heads + head) * e.seq + tok) * e.d_head + d) * ES : kOob;
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) bstore(c.aux0, off[r], 0, acc[4 * g + r] + bias, static_cast<T*>(nullptr));
-      }
-    } else {
-      // values: the cache holds them transposed, [slot, head, d, token]; the
-      // optional copy keeps token rows, [slot, head, token, d]
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int m0 = m_tile + 8 * g + rq;
-        float x[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) x[r] = acc[4 * g + r] + bias;
-        if (!e.idx && (e.per_slot & 3) == 0) {
-          // dense rows m0..m0+3 are four consecutive tokens of one slot
-          const int slot = div_by(m0, e.slot_magic, e.slot_shift);
-          const int tok = m0 - slot * e.per_slot;
-          const int off = (n_ok && m0 < M) ? (((slot * e.n_heads + head) * e.d_head + d) * e.seq + tok) * ES : kOob;
-          if constexpr (ES == 2) {
-            const uint32_t lo = pack2bf(x[0], x[1]), hi = pack2bf(x[2], x[3]);
-            __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{lo, hi}, c.aux1, off, 0, 0);
-          } else {
-            __builtin_amdgcn_raw_buffer_store_b128(
-                u32x4_t{__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]), __float_as_uint(x[3])},
-                c.aux1, off, 0, 0);
-          }
-          if (e.v_copy) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int offc = (n_ok && m0 < M) ? (((slot * e.n_heads + head) * e.seq + tok + r) * e.d_head + d) * ES : kOob;
-              bstore(c.aux2, offc, 0, x[r], static_cast<T*>(nullptr));
-            }
-          }
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int m = m0 + r;
-            const int mc = min(m, M - 1);
-            const int slot = div_by(mc, e.slot_magic, e.slot_shift);
-            const int tok = e.idx ? e.idx[mc] : mc - slot * e.per_slot;
-            const bool ok = n_ok && m < M;
-            bstore(c.aux1, ok ? (((slot * e.n_heads + head) * e.d_head + d) * e.seq + tok) * ES : kOob, 0, x[r],
-                   static_cast<T*>(nullptr));
-            if (e.v_copy)
-              bstore(c.aux2, ok ? (((slot * e.n_heads + head) * e.seq + tok) * e.d_head + d) * ES : kOob, 0, x[r],
-                     static_cast<T*>(nullptr));
-          }
-        }
-      }
-    }
-  }
-}
 
 template <typename T, int KIND>
 __device__ __forceinline__ EpiCtx<T, KIND> make_epi(const EpiArgs& e, int M, int N) {
@@ -299,6 +188,107 @@ __device__ __forceinline__ EpiCtx<T, KIND> make_epi(const EpiArgs& e, int M, int
   return c;
 }
 
+// QKV column section of global column ng: 0 query, 1 key, 2 value
+__device__ __forceinline__ int qkv_section(const EpiArgs& e, int ng) {
+  return ng >= 2 * e.d_model ? 2 : (ng >= e.d_model ? 1 : 0);
+}
+
+// Epilogue of one 32-row strip of a wave's tile: rows m_strip + 0..31,
+// columns n_wave + 0..WN-1; sb is the bias of those columns (LDS), reg the
+// wave's LDS staging region (32 * WN * 4 bytes).
+template <typename T, int KIND, int WN>
+__device__ __forceinline__ void epilogue_strip(const EpiArgs& e, const EpiCtx<T, KIND>& c, int M, int N,
+                                               int m_strip, int n_wave, int lane, const float* sb,
+                                               const f32x16_t (&acc)[WN / 32], unsigned char* reg) {
+  constexpr int TN = WN / 32;
+  typedef typename std::conditional<KIND == EPI_RESIDUAL, float, T>::type OT;  // output type
+  constexpr int OS = sizeof(OT);
+  constexpr int RB = WN * OS;        // bytes per staged row
+  constexpr int NCH = RB / 16;       // 16-byte chunks per row
+  constexpr int COLS = 16 / OS;      // columns per chunk
+  static_assert((NCH & (NCH - 1)) == 0 && (32 * NCH) % 64 == 0, "chunks per staged row");
+  const int row = lane & 31, h4 = (lane >> 5) * 4;
+
+  // 1. bias (+ activation) in registers, rows into LDS; chunk c of row r sits
+  //    at chunk c ^ (r % NCH), which spreads a wave's accesses over the banks
+  bool any_v = false;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    float x[4][4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x4_t bv = *reinterpret_cast<const f32x4_t*>(sb + 32 * j + 8 * g + h4);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        x[g][r] = acc[j][4 * g + r] + bv[r];
+        if constexpr (KIND == EPI_GELU) x[g][r] = gelu_erf(x[g][r]);
+      }
+      const int colb = (32 * j + 8 * g + h4) * OS;
+      lds_put4(reg + row * RB + ((((colb >> 4) ^ row) & (NCH - 1)) << 4) + (colb & 15), x[g],
+               static_cast<OT*>(nullptr));
+    }
+    if constexpr (KIND == EPI_QKV) {
+      // value columns: the transposed cache [slot, head, d, tok] takes one
+      // element per store, straight from registers (lanes of consecutive
+      // rows write consecutive tokens)
+      const int ng0 = n_wave + 32 * j + e.n_offset;
+      if (qkv_section(e, ng0) == 2 && e.v_cache) {
+        const int m = m_strip + row;
+        const int mc = min(m, M - 1);
+        const int slot = div_by(mc, e.slot_magic, e.slot_shift);
+        const int tok = e.idx ? e.idx[mc] : mc - slot * e.per_slot;
+        const int vrow = slot * e.n_heads * e.d_head * e.seq + tok;
+        const int rem0 = ng0 - 2 * e.d_model;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const bool ok = m < M && n_wave + 32 * j + 8 * g + h4 < N;
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            bstore1(c.aux1, ok ? (vrow + (rem0 + 8 * g + h4 + r) * e.seq) * OS : kOob, x[g][r],
+                    static_cast<OT*>(nullptr));
+        }
+      }
+      any_v = any_v || qkv_section(e, ng0) == 2;
+    }
+  }
+
+  // 2. 16-byte chunks back out of LDS, eight lanes per 128 bytes of a row
+#pragma unroll
+  for (int it = 0; it < 32 * NCH / 64; ++it) {
+    const int v = lane + 64 * it;
+    const int r = v / NCH, ch = v & (NCH - 1);
+    const u32x4_t val = *reinterpret_cast<const u32x4_t*>(reg + r * RB + (((ch ^ r) & (NCH - 1)) << 4));
+    const int m = m_strip + r;
+    const int n = n_wave + ch * COLS;
+    const bool ok = m < M && n < N;
+    const int mc = min(m, M - 1);
+    if constexpr (KIND == EPI_BIAS || KIND == EPI_GELU) {
+      bstore16(c.out, ok ? (mc * N + n) * OS : kOob, val);
+    } else if constexpr (KIND == EPI_RESIDUAL) {
+      const int lin = ok ? (mc * N + n) * 4 : kOob;
+      const u32x4_t res = bload16(c.aux0, lin);
+      u32x4_t y;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) y[q] = __float_as_uint(__uint_as_float(res[q]) + __uint_as_float(val[q]));
+      const int orow = e.out_idx ? div_by(mc, e.slot_magic, e.slot_shift) * e.seq + e.out_idx[mc] : mc;
+      bstore16(c.out, ok ? (orow * N + n) * 4 : kOob, y);
+      if (e.resid_copy) bstore16(c.aux1, lin, y);
+    } else {
+      const int ng = n + e.n_offset;
+      const int sec = qkv_section(e, ng);
+      const int rem = ng - sec * e.d_model;  // head * d_head + d
+      const int slot = div_by(mc, e.slot_magic, e.slot_shift);
+      const int tok = e.idx ? e.idx[mc] : mc - slot * e.per_slot;
+      const int head = div_by(rem, e.head_magic, e.head_shift);
+      // [slot, head, tok, d]
+      const int krow = ((slot * e.n_heads + head) * e.seq + tok) * e.d_head + (rem - head * e.d_head);
+      bstore16(c.out, ok && sec == 0 ? (mc * e.d_model + rem) * OS : kOob, val);
+      bstore16(c.aux0, ok && sec == 1 ? krow * OS : kOob, val);
+      if (any_v && e.v_copy) bstore16(c.aux2, ok && sec == 2 ? krow * OS : kOob, val);
+    }
+  }
+}
+
 // Tile BM x BN, WAVES_M x WAVES_N waves, each wave (BM / WAVES_M) x
 // (BN / WAVES_N); STAGES LDS buffers of (BM + BN) rows x 128 bytes.
 template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int KIND>
@@ -317,11 +307,11 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   static_assert(A_INSTR * 8 * NW == BM && B_INSTR * 8 * NW == BN, "tile/waves");
   static_assert(STAGES >= 2 && STAGES <= 4, "stages");
 
-  __shared__ __align__(1024) unsigned char s0[STAGE_BYTES];
-  __shared__ __align__(1024) unsigned char s1[STAGE_BYTES];
-  __shared__ __align__(1024) unsigned char s2[STAGES > 2 ? STAGE_BYTES : 16];
-  __shared__ __align__(1024) unsigned char s3[STAGES > 3 ? STAGE_BYTES : 16];
-  unsigned char* const stage[4] = {s0, s1, s2, s3};
+  __shared__ __align__(1024) unsigned char ring[STAGES * STAGE_BYTES];
+  __shared__ __align__(16) float sbias[BN];
+  // epilogue staging: one region of 32 rows x WN fp32 per wave, in the ring
+  constexpr int REGION = 32 * WN * 4;
+  static_assert(NW * REGION <= STAGES * STAGE_BYTES, "epilogue staging fits the ring");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -332,13 +322,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   const int tile_n = blockIdx.x - tile_m * tiles_n;
   const int m_base = tile_m * BM;
   const int n_base = tile_n * BN;
-  const int col = lane & 31;
-  const int rq = (lane >> 5) * 4;
 
-  // epilogue bias of this lane's columns, fetched before the main loop
-  float bias[TN];
-#pragma unroll
-  for (int j = 0; j < TN; ++j) bias[j] = e.bias[min(n_base + wn * WN + j * 32 + col, N - 1)];
+  // the tile's bias, visible to the epilogue after the main loop's barriers
+  for (int t = tid; t < BN; t += 64 * NW) sbias[t] = e.bias[min(n_base + t, N - 1)];
 
   const int Kb = K * static_cast<int>(sizeof(T));
   const i32x4_t ra = make_rsrc(A + static_cast<long>(m_base) * K,
@@ -402,12 +388,12 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) Mma<T>::run(acc[i][j], fa[cur][i], fb[cur][j]);
+        for (int j = 0; j < TN; ++j) Mma<T>::run(acc[i][j], fb[cur][j], fa[cur][i]);  // C^T tile
     }
   };
 
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s) issue(stage[s], s);
+  for (int s = 0; s < STAGES - 1; ++s) issue(ring + s * STAGE_BYTES, s);
   for (int kt0 = 0; kt0 < KT; kt0 += STAGES) {
 #pragma unroll
     for (int u = 0; u < STAGES; ++u) {
@@ -419,94 +405,23 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
         __builtin_amdgcn_s_barrier();
         // the buffer of slice kt-1 is free: every wave passed the barrier
         // after reading it
-        issue(stage[(u + STAGES - 1) % STAGES], kt + STAGES - 1);
-        compute(stage[u]);
+        issue(ring + ((u + STAGES - 1) % STAGES) * STAGE_BYTES, kt + STAGES - 1);
+        compute(ring + u * STAGE_BYTES);
       }
     }
   }
   wait_vm<0>();  // no load may still target this workgroup's LDS
 
+  __syncthreads();  // every wave is done with the ring: it becomes staging space
+
   const EpiCtx<T, KIND> ec = make_epi<T, KIND>(e, M, N);
-  if constexpr (KIND == EPI_QKV && sizeof(T) == 2) {
-    // Dense value columns go to the transposed cache through LDS, so that
-    // each lane stores 16 bytes of consecutive tokens of one dimension.  A
-    // wave stages its WN x WM tile as rows of dimensions (WM tokens each),
-    // 16-byte chunks XOR-swizzled by the row so that writes and reads spread
-    // over the banks; a wave's region never straddles two ring buffers.
-    constexpr int ROWB_V = WM * 2;                      // bytes per staged row
-    constexpr int NCH = ROWB_V / 16;                    // chunks per row
-    constexpr int REGION = WN * ROWB_V;
-    constexpr int PER_BUF = STAGE_BYTES / REGION;       // wave regions per ring buffer
-    static_assert(PER_BUF >= 1 && (NW + PER_BUF - 1) / PER_BUF <= STAGES, "value staging fits the LDS ring");
-    static_assert((NCH & (NCH - 1)) == 0, "power-of-two chunks per row");
-    if (!e.idx && (e.per_slot & 7) == 0) {
-      __syncthreads();  // every wave is done with the LDS ring
-      const int n_wave = n_base + wn * WN;
-      const bool wave_v = n_wave < N && (n_wave + e.n_offset) / e.d_model == 2;
-      if (wave_v) {
-        const int bufi = wave / PER_BUF;
-        unsigned char* reg = (bufi == 0 ? s0 : bufi == 1 ? s1 : bufi == 2 ? s2 : s3) + (wave % PER_BUF) * REGION;
-        auto at = [&](int row, int byte) {  // byte offset within the row
-          return reg + row * ROWB_V + ((((byte >> 4) ^ row) & (NCH - 1)) << 4) + (byte & 15);
-        };
-        // acc[i][j][4 g + r]: token row wm*WM + 32 i + 8 g + rq + r, d column 32 j + col
+  unsigned char* const reg = ring + wave * REGION;
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-              const float bj = bias[j];
-              const u32x2_t w = {pack2bf(acc[i][j][4 * g] + bj, acc[i][j][4 * g + 1] + bj),
-                                 pack2bf(acc[i][j][4 * g + 2] + bj, acc[i][j][4 * g + 3] + bj)};
-              *reinterpret_cast<u32x2_t*>(at(32 * j + col, (32 * i + 8 * g + rq) * 2)) = w;
-            }
-        // read back 16-byte runs of 8 tokens: WN rows x WM / 8 chunks
-        const int rem0 = (n_wave + e.n_offset) - 2 * e.d_model;
-        constexpr int CHUNKS = WN * (WM / 8);
-#pragma unroll
-        for (int it = 0; it < CHUNKS / 64; ++it) {
-          const int v = lane + 64 * it;
-          const int dl = v / (WM / 8), c = v - dl * (WM / 8);
-          const u32x4_t val = *reinterpret_cast<const u32x4_t*>(at(dl, c * 16));
-          const int m = m_base + wm * WM + 8 * c;
-          const int rem = rem0 + dl;
-          const int head = rem / e.d_head, d = rem - head * e.d_head;
-          const int slot = div_by(m, e.slot_magic, e.slot_shift), tok = m - slot * e.per_slot;
-          const int off = (m < M && n_wave + dl < N)
-                              ? (((slot * e.n_heads + head) * e.d_head + d) * e.seq + tok) * 2 : kOob;
-          __builtin_amdgcn_raw_buffer_store_b128(val, ec.aux1, off, 0, 0);
-        }
-        if (e.v_copy) {  // token rows as well (the scoring block)
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-#pragma unroll
-              for (int g = 0; g < 4; ++g)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                  const int m = m_base + wm * WM + 32 * i + 8 * g + rq + r;
-                  const int rem = rem0 + 32 * j + col;
-                  const int head = rem / e.d_head, d = rem - head * e.d_head;
-                  const int slot = div_by(m, e.slot_magic, e.slot_shift), tok = m - slot * e.per_slot;
-                  const int off = (m < M && n_wave + 32 * j + col < N)
-                                      ? (((slot * e.n_heads + head) * e.seq + tok) * e.d_head + d) * 2 : kOob;
-                  bstore(ec.aux2, off, 0, acc[i][j][4 * g + r] + bias[j], static_cast<T*>(nullptr));
-                }
-        }
-        return;
-      }
-    }
+  for (int i = 0; i < TM; ++i) {
+    epilogue_strip<T, KIND, WN>(e, ec, M, N, m_base + wm * WM + 32 * i, n_base + wn * WN, lane,
+                                sbias + wn * WN, acc[i], reg);
+    __builtin_amdgcn_sched_barrier(0);
   }
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      epilogue_tile<T, KIND>(e, ec, M, N, m_base + wm * WM + i * 32, rq, n_base + wn * WN + j * 32 + col,
-                             bias[j], acc[i][j]);
-      __builtin_amdgcn_sched_barrier(0);  // keep each tile's loads with its stores
-    }
 }
 
 template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int KIND>
@@ -562,12 +477,19 @@ void set_gemm_variant(int v) { g_gemm_variant = v; }
 hipError_t launch_gemm(int dtype, const void* A, const void* W, int M, int N, int K,
                        const EpiArgs& e_in, hipStream_t st) {
   if (M == 0 || N == 0) return hipSuccess;
+  if (N % 8) return hipErrorInvalidValue;  // epilogue stores whole 16-byte chunks
   EpiArgs e = e_in;
   if (e.kind == EPI_QKV || (e.kind == EPI_RESIDUAL && e.out_idx)) {
     if (e.per_slot < 1) return hipErrorInvalidValue;
     const Divisor dv = make_divisor(static_cast<uint32_t>(e.per_slot));
     e.slot_magic = dv.magic;
     e.slot_shift = dv.shift;
+  }
+  if (e.kind == EPI_QKV) {
+    if (e.d_head < 1 || e.d_model % 32 || e.n_offset % 32) return hipErrorInvalidValue;
+    const Divisor dh = make_divisor(static_cast<uint32_t>(e.d_head));
+    e.head_magic = dh.magic;
+    e.head_shift = dh.shift;
   }
   // 32-bit buffer offsets: a tile's operand rows and every output must span
   // less than 2 GiB
