@@ -1,4 +1,6 @@
 """Host logic: the period schedule of Sec. 4.1 and the FLOP model."""
+import os
+
 import pytest
 
 from paper_2503_12450_amd import flops, schedule
@@ -51,12 +53,26 @@ def test_flop_model_closed_forms():
     assert abs(c / 1e12 - 4.084) < 0.01
 
 
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _table1():
+    """{model: (64-step, 32-step, 16-step) TFLOPs} as Table 1 prints them."""
+    rows = {}
+    with open(os.path.join(GOLDEN, "table1_mar_baseline_flops.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                model, steps, tf = line.split()
+                rows.setdefault(model, {})[int(steps)] = float(tf)
+    return {m: (v[64], v[32], v[16]) for m, v in rows.items()}
+
+
 def test_table1_baseline_flops_are_linear_in_steps():
     # Table 1: MAR baselines at 64/32/16 decoding steps (T FLOPs per image).
     # The per-step slope is a fixed fraction of the fixed-length transformer
     # (both guidance pathways, 320 tokens through every block), the same for
     # the three model sizes.
-    table = {"mar-b": (15.49, 9.54, 6.51), "mar-l": (35.05, 21.15, 14.20), "mar-h": (69.06, 42.12, 28.67)}
+    table = _table1()
     ratios = []
     for key, (f64, f32, f16) in table.items():
         slope = (f64 - f32) / 32
