@@ -111,8 +111,6 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-// physical 16-byte chunk of logical chunk c in LDS row r
-__device__ __forceinline__ int swz(int row, int c) { return c ^ ((row >> 1) & 7); }
 
 // ---------------------------------------------------------------------------
 // Epilogues.  The MFMA forms C^T = W A^T (weight fragment as its first
@@ -289,23 +287,51 @@ __device__ __forceinline__ void epilogue_strip(const EpiArgs& e, const EpiCtx<T,
   }
 }
 
+// Workgroup -> output tile.  Workgroups are dispatched round-robin over the
+// eight XCDs (workgroup b runs on XCD b % 8), and each XCD has its own L2.
+// Each XCD is given a contiguous range of the tile order, and that order
+// walks kGroupM row tiles before moving to the next column tile, so the
+// ~32 workgroups an XCD runs at once share 4 row tiles of A and 8 column
+// tiles of W instead of touching every row tile of A.  The map is a
+// bijection for any tile count.
+constexpr int kXcds = 8;
+constexpr int kGroupM = 4;
+__device__ __forceinline__ void tile_of(int b, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int total = tiles_m * tiles_n;
+  const int q = total / kXcds, r = total - q * kXcds;
+  const int x = b % kXcds, l = b / kXcds;
+  const int t = x * q + min(x, r) + l;  // position in the tile order
+  const int group = kGroupM * tiles_n;
+  const int g = t / group, first_m = g * kGroupM;
+  const int gm = min(tiles_m - first_m, kGroupM);
+  const int in = t - g * group;
+  tm = first_m + in % gm;
+  tn = in / gm;
+}
+
 // Tile BM x BN, WAVES_M x WAVES_N waves, each wave (BM / WAVES_M) x
-// (BN / WAVES_N); STAGES LDS buffers of (BM + BN) rows x 128 bytes.
-template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int KIND>
+// (BN / WAVES_N); STAGES LDS buffers of (BM + BN) rows x ROWB bytes of K.
+// Within a row the 16-byte chunks are XOR-swizzled by (row / RPB) % NCH,
+// RPB = 256 / ROWB rows per 256 bytes of banks: the 16 lanes of one LDS
+// read phase (16 rows, one chunk each) then hit 16 distinct bank groups.
+template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int ROWB, int KIND>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* __restrict__ A,
                                                                     const T* __restrict__ W, int M,
                                                                     int N, int K, EpiArgs e) {
   constexpr int NW = WAVES_M * WAVES_N;
-  constexpr int ROWB = 128;                    // bytes of K per LDS row and slice
   constexpr int STAGE_BYTES = (BM + BN) * ROWB;
-  constexpr int A_INSTR = BM / 8 / NW;         // 8 rows (1 KiB) per wave-wide load
-  constexpr int B_INSTR = BN / 8 / NW;
+  constexpr int NCH = ROWB / 16;               // 16-byte chunks per row
+  constexpr int RPB = 256 / ROWB;              // rows per 256 bytes
+  constexpr int RPI = 1024 / ROWB;             // rows per wave-wide (1 KiB) load
+  constexpr int A_INSTR = BM / RPI / NW;
+  constexpr int B_INSTR = BN / RPI / NW;
   constexpr int LOADS = A_INSTR + B_INSTR;     // loads per wave per slice
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int KSTEPS = ROWB / 32;            // MFMA k-steps per slice
-  static_assert(A_INSTR * 8 * NW == BM && B_INSTR * 8 * NW == BN, "tile/waves");
-  static_assert(STAGES >= 2 && STAGES <= 4, "stages");
+  static_assert(ROWB == 64 || ROWB == 128, "slice width");
+  static_assert(A_INSTR * RPI * NW == BM && B_INSTR * RPI * NW == BN, "tile/waves");
+  static_assert(STAGES >= 2 && STAGES <= 5, "stages");
 
   __shared__ __align__(1024) unsigned char ring[STAGES * STAGE_BYTES];
   __shared__ __align__(16) float sbias[BN];
@@ -317,9 +343,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave - (wave / WAVES_N) * WAVES_N;
-  const int tiles_n = (N + BN - 1) / BN;
-  const int tile_m = blockIdx.x / tiles_n;
-  const int tile_n = blockIdx.x - tile_m * tiles_n;
+  int tile_m, tile_n;
+  tile_of(blockIdx.x, (M + BM - 1) / BM, (N + BN - 1) / BN, tile_m, tile_n);
   const int m_base = tile_m * BM;
   const int n_base = tile_n * BN;
 
@@ -331,25 +356,33 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
                                static_cast<unsigned>(min(BM, M - m_base)) * Kb);
   const i32x4_t rb = make_rsrc(W + static_cast<long>(n_base) * K,
                                static_cast<unsigned>(min(BN, N - n_base)) * Kb);
-  const int KT = Kb / ROWB;
-  // lane's place in a wave-wide load: row r_in of 8, physical chunk pc
-  const int r_in = lane >> 3, pc = lane & 7;
-  auto issue = [&](unsigned char* st, int kt) {
+  const int KT = Kb / ROWB;  // K * sizeof(T) is a multiple of 128
+  // A wave-wide load moves RPI rows (group grp) of one slice: lane -> row
+  // grp*RPI + r_in, physical chunk pc.  The row's swizzle is
+  // (4 grp + r_in / RPB) % NCH, so two lane offsets (even and odd groups)
+  // serve every group; the group's row offset is wave-uniform and rides in
+  // the scalar offset.
+  static_assert(A_INSTR % 2 == 0 && B_INSTR % 2 == 0, "load groups come in pairs");
+  const int r_in = lane / NCH, pc = lane % NCH;
+  const int voff[2] = {r_in * Kb + ((pc ^ ((r_in / RPB) % NCH)) << 4),
+                       r_in * Kb + ((pc ^ ((4 + r_in / RPB) % NCH)) << 4)};
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  // load q of a slice's LOADS wave-wide loads (A rows first, then W rows)
+  auto issue_one = [&](unsigned char* st, int kt, int q) {
     const int kb = kt < KT ? kt * ROWB : 0;  // past the end: a harmless reload of slice 0
-#pragma unroll
-    for (int i = 0; i < A_INSTR; ++i) {
-      const int grp = wave * A_INSTR + i;
-      const int row = grp * 8 + r_in;
-      dma16(ra, static_cast<unsigned>(reinterpret_cast<uintptr_t>(st + grp * 1024)),
-            row * Kb + swz(row, pc) * 16, kb);
-    }
-#pragma unroll
-    for (int i = 0; i < B_INSTR; ++i) {
-      const int grp = wave * B_INSTR + i;
-      const int row = grp * 8 + r_in;
+    if (q < A_INSTR) {
+      const int grp = wave_u * A_INSTR + q;
+      dma16(ra, static_cast<unsigned>(reinterpret_cast<uintptr_t>(st + grp * 1024)), voff[q & 1],
+            kb + grp * RPI * Kb);
+    } else {
+      const int grp = wave_u * B_INSTR + (q - A_INSTR);
       dma16(rb, static_cast<unsigned>(reinterpret_cast<uintptr_t>(st + BM * ROWB + grp * 1024)),
-            row * Kb + swz(row, pc) * 16, kb);
+            voff[(q - A_INSTR) & 1], kb + grp * RPI * Kb);
     }
+  };
+  auto issue = [&](unsigned char* st, int kt) {
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) issue_one(st, kt, q);
   };
 
   f32x16_t acc[TM][TN];
@@ -360,17 +393,29 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int frow = lane & 31, fch = lane >> 5;
+  // fragment reads: lane -> row frow of a 32-row tile, 16-byte chunk
+  // 2*kk + fch.  Tile rows start at multiples of 32, so the swizzle is
+  // (frow / RPB) % NCH for every tile and the offsets per k-step are shared
+  // by all tiles (the tile's row offset is an immediate).
+  const int frow = lane & 31, fch = lane >> 5, fsw = (frow / RPB) % NCH;
+  int a_off[KSTEPS], b_off[KSTEPS];
+#pragma unroll
+  for (int kk = 0; kk < KSTEPS; ++kk) {
+    a_off[kk] = (wm * WM + frow) * ROWB + (((2 * kk + fch) ^ fsw) << 4);
+    b_off[kk] = BM * ROWB + (wn * WN + frow) * ROWB + (((2 * kk + fch) ^ fsw) << 4);
+  }
   auto frag_a = [&](const unsigned char* st, int i, int kk) {
-    const int row = wm * WM + i * 32 + frow;
-    return *reinterpret_cast<const u32x4_t*>(st + row * ROWB + swz(row, 2 * kk + fch) * 16);
+    return *reinterpret_cast<const u32x4_t*>(st + a_off[kk] + i * 32 * ROWB);
   };
   auto frag_b = [&](const unsigned char* st, int j, int kk) {
-    const int row = wn * WN + j * 32 + frow;
-    return *reinterpret_cast<const u32x4_t*>(st + BM * ROWB + row * ROWB + swz(row, 2 * kk + fch) * 16);
+    return *reinterpret_cast<const u32x4_t*>(st + b_off[kk] + j * 32 * ROWB);
   };
-  // fragments of k-step kk+1 are read while k-step kk multiplies
-  auto compute = [&](const unsigned char* st) {
+  // Fragments of k-step kk+1 are read while k-step kk multiplies, and the
+  // loads of slice kt_next into buffer nst are spread over the k-steps: a
+  // wave that issued all of them at once would queue behind every other
+  // wave's loads before reaching its first MFMA.
+  constexpr int PER_STEP = (LOADS + KSTEPS - 1) / KSTEPS;
+  auto compute = [&](const unsigned char* st, unsigned char* nst, int kt_next) {
     u32x4_t fa[2][TM], fb[2][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i) fa[0][i] = frag_a(st, i, 0);
@@ -385,6 +430,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
 #pragma unroll
         for (int j = 0; j < TN; ++j) fb[cur ^ 1][j] = frag_b(st, j, kk + 1);
       }
+#pragma unroll
+      for (int q = kk * PER_STEP; q < (kk + 1) * PER_STEP && q < LOADS; ++q) issue_one(nst, kt_next, q);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -403,10 +450,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
         // its own loads (one load group per slice is issued per iteration)
         wait_vm<LOADS * (STAGES - 2)>();
         __builtin_amdgcn_s_barrier();
-        // the buffer of slice kt-1 is free: every wave passed the barrier
-        // after reading it
-        issue(ring + ((u + STAGES - 1) % STAGES) * STAGE_BYTES, kt + STAGES - 1);
-        compute(ring + u * STAGE_BYTES);
+        // the buffer of slice kt-1 is free (every wave passed the barrier
+        // after reading it): it receives slice kt+STAGES-1 during compute
+        compute(ring + u * STAGE_BYTES, ring + ((u + STAGES - 1) % STAGES) * STAGE_BYTES, kt + STAGES - 1);
       }
     }
   }
@@ -424,11 +470,11 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   }
 }
 
-template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int KIND>
+template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int ROWB, int KIND>
 static hipError_t gemm_launch(const void* A, const void* W, int M, int N, int K,
                               const EpiArgs& e, hipStream_t st) {
   const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WAVES_M, WAVES_N, STAGES, KIND>), dim3(tiles),
+  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WAVES_M, WAVES_N, STAGES, ROWB, KIND>), dim3(tiles),
                      dim3(64 * WAVES_M * WAVES_N), 0, st, static_cast<const T*>(A),
                      static_cast<const T*>(W), M, N, K, e);
   return hipGetLastError();
@@ -443,20 +489,28 @@ static hipError_t gemm_pick(const void* A, const void* W, int M, int N, int K, c
                             hipStream_t st) {
   int v = g_gemm_variant;
   if (v < 0) {
-    // (measured on MI355X) 128 x 128 tiles with a 3-deep prefetch when each
-    // CU gets at most one of them; otherwise 256 x 256 tiles once there are
-    // at least half as many as CUs, and 128 x 128 tiles with two workgroups
-    // per CU below that
+    // measured on MI355X over the block's shapes (d_model 1024, M from 3200
+    // to 40960): the fp32 residual products are epilogue-heavy and prefer
+    // 128-row tiles (128 x 256 once K is long and there are enough of
+    // them); the others take 256 x 256 tiles with a 4-deep ring of 64-byte
+    // slices, except in the middle range where two 128 x 128 workgroups
+    // per CU balance better
     const long big = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
     const long small = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
-    v = small <= 256 ? 1 : (big >= 128 ? 0 : 4);
+    if (small <= 256)
+      v = 1;
+    else if (KIND == EPI_RESIDUAL)
+      v = (K >= 2048 && big >= 256) ? 3 : 4;
+    else
+      v = (big > 256 && big <= 512) ? 4 : 5;
   }
   switch (v) {
-    case 0: return gemm_launch<T, 256, 256, 2, 4, 2, KIND>(A, W, M, N, K, e, st);
-    case 1: return gemm_launch<T, 128, 128, 2, 2, 3, KIND>(A, W, M, N, K, e, st);
-    case 2: return gemm_launch<T, 256, 128, 2, 2, 3, KIND>(A, W, M, N, K, e, st);
-    case 3: return gemm_launch<T, 128, 256, 2, 2, 3, KIND>(A, W, M, N, K, e, st);
-    default: return gemm_launch<T, 128, 128, 2, 2, 2, KIND>(A, W, M, N, K, e, st);
+    case 0: return gemm_launch<T, 256, 256, 2, 4, 2, 128, KIND>(A, W, M, N, K, e, st);
+    case 1: return gemm_launch<T, 128, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, st);
+    case 2: return gemm_launch<T, 256, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, st);
+    case 3: return gemm_launch<T, 128, 256, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, st);
+    case 5: return gemm_launch<T, 256, 256, 2, 4, 4, 64, KIND>(A, W, M, N, K, e, st);
+    default: return gemm_launch<T, 128, 128, 2, 2, 2, 128, KIND>(A, W, M, N, K, e, st);
   }
 }
 
