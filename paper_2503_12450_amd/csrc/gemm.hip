@@ -98,8 +98,7 @@ __device__ __forceinline__ i32x4_t make_rsrc(const void* base, unsigned bytes) {
 __device__ __forceinline__ void dma16(i32x4_t rsrc, unsigned lds_addr, int voff, int soff) {
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
                :
-               : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(rsrc),
-                 "s"(__builtin_amdgcn_readfirstlane(soff))
+               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
                : "memory", "m0");
 }
 #pragma clang diagnostic pop
@@ -319,7 +318,11 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
                                                                     const T* __restrict__ W, int M,
                                                                     int N, int K, EpiArgs e) {
   constexpr int NW = WAVES_M * WAVES_N;
-  constexpr int STAGE_BYTES = (BM + BN) * ROWB;
+  // LDS: the A rows of all stages, then the W rows of all stages, so that a
+  // fragment's stage and tile offsets fit the 16-bit immediate of ds_read
+  constexpr int A_BYTES = BM * ROWB, B_BYTES = BN * ROWB;
+  constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+  constexpr int B_RING = STAGES * A_BYTES;
   constexpr int NCH = ROWB / 16;               // 16-byte chunks per row
   constexpr int RPB = 256 / ROWB;              // rows per 256 bytes
   constexpr int RPI = 1024 / ROWB;             // rows per wave-wide (1 KiB) load
@@ -367,22 +370,26 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   const int voff[2] = {r_in * Kb + ((pc ^ ((r_in / RPB) % NCH)) << 4),
                        r_in * Kb + ((pc ^ ((4 + r_in / RPB) % NCH)) << 4)};
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-  // load q of a slice's LOADS wave-wide loads (A rows first, then W rows)
-  auto issue_one = [&](unsigned char* st, int kt, int q) {
+  // Load q of a slice's LOADS wave-wide loads (A rows first, then W rows)
+  // into ring stage su.  Every operand but the lane offset is wave-uniform
+  // and computed from readfirstlane'd values, so it stays in SGPRs.
+  const unsigned lds_ring = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(
+      static_cast<int>(reinterpret_cast<uintptr_t>(static_cast<unsigned char*>(ring)))));
+  const int Kb_u = __builtin_amdgcn_readfirstlane(Kb);
+  auto issue_one = [&](int su, int kt, int q) {
     const int kb = kt < KT ? kt * ROWB : 0;  // past the end: a harmless reload of slice 0
     if (q < A_INSTR) {
       const int grp = wave_u * A_INSTR + q;
-      dma16(ra, static_cast<unsigned>(reinterpret_cast<uintptr_t>(st + grp * 1024)), voff[q & 1],
-            kb + grp * RPI * Kb);
+      dma16(ra, lds_ring + su * A_BYTES + grp * 1024, voff[q & 1], kb + grp * RPI * Kb_u);
     } else {
       const int grp = wave_u * B_INSTR + (q - A_INSTR);
-      dma16(rb, static_cast<unsigned>(reinterpret_cast<uintptr_t>(st + BM * ROWB + grp * 1024)),
-            voff[(q - A_INSTR) & 1], kb + grp * RPI * Kb);
+      dma16(rb, lds_ring + B_RING + su * B_BYTES + grp * 1024, voff[(q - A_INSTR) & 1],
+            kb + grp * RPI * Kb_u);
     }
   };
-  auto issue = [&](unsigned char* st, int kt) {
+  auto issue = [&](int su, int kt) {
 #pragma unroll
-    for (int q = 0; q < LOADS; ++q) issue_one(st, kt, q);
+    for (int q = 0; q < LOADS; ++q) issue_one(su, kt, q);
   };
 
   f32x16_t acc[TM][TN];
@@ -402,36 +409,36 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
 #pragma unroll
   for (int kk = 0; kk < KSTEPS; ++kk) {
     a_off[kk] = (wm * WM + frow) * ROWB + (((2 * kk + fch) ^ fsw) << 4);
-    b_off[kk] = BM * ROWB + (wn * WN + frow) * ROWB + (((2 * kk + fch) ^ fsw) << 4);
+    b_off[kk] = B_RING + (wn * WN + frow) * ROWB + (((2 * kk + fch) ^ fsw) << 4);
   }
-  auto frag_a = [&](const unsigned char* st, int i, int kk) {
-    return *reinterpret_cast<const u32x4_t*>(st + a_off[kk] + i * 32 * ROWB);
+  auto frag_a = [&](int su, int i, int kk) {
+    return *reinterpret_cast<const u32x4_t*>(ring + a_off[kk] + su * A_BYTES + i * 32 * ROWB);
   };
-  auto frag_b = [&](const unsigned char* st, int j, int kk) {
-    return *reinterpret_cast<const u32x4_t*>(st + b_off[kk] + j * 32 * ROWB);
+  auto frag_b = [&](int su, int j, int kk) {
+    return *reinterpret_cast<const u32x4_t*>(ring + b_off[kk] + su * B_BYTES + j * 32 * ROWB);
   };
   // Fragments of k-step kk+1 are read while k-step kk multiplies, and the
   // loads of slice kt_next into buffer nst are spread over the k-steps: a
   // wave that issued all of them at once would queue behind every other
   // wave's loads before reaching its first MFMA.
   constexpr int PER_STEP = (LOADS + KSTEPS - 1) / KSTEPS;
-  auto compute = [&](const unsigned char* st, unsigned char* nst, int kt_next) {
+  auto compute = [&](int su, int nsu, int kt_next) {
     u32x4_t fa[2][TM], fb[2][TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i) fa[0][i] = frag_a(st, i, 0);
+    for (int i = 0; i < TM; ++i) fa[0][i] = frag_a(su, i, 0);
 #pragma unroll
-    for (int j = 0; j < TN; ++j) fb[0][j] = frag_b(st, j, 0);
+    for (int j = 0; j < TN; ++j) fb[0][j] = frag_b(su, j, 0);
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; ++kk) {
       const int cur = kk & 1;
       if (kk + 1 < KSTEPS) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i) fa[cur ^ 1][i] = frag_a(st, i, kk + 1);
+        for (int i = 0; i < TM; ++i) fa[cur ^ 1][i] = frag_a(su, i, kk + 1);
 #pragma unroll
-        for (int j = 0; j < TN; ++j) fb[cur ^ 1][j] = frag_b(st, j, kk + 1);
+        for (int j = 0; j < TN; ++j) fb[cur ^ 1][j] = frag_b(su, j, kk + 1);
       }
 #pragma unroll
-      for (int q = kk * PER_STEP; q < (kk + 1) * PER_STEP && q < LOADS; ++q) issue_one(nst, kt_next, q);
+      for (int q = kk * PER_STEP; q < (kk + 1) * PER_STEP && q < LOADS; ++q) issue_one(nsu, kt_next, q);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -440,21 +447,20 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   };
 
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s) issue(ring + s * STAGE_BYTES, s);
-  for (int kt0 = 0; kt0 < KT; kt0 += STAGES) {
-#pragma unroll
-    for (int u = 0; u < STAGES; ++u) {
-      const int kt = kt0 + u;
-      if (kt < KT) {
-        // every wave's slice kt has landed once each wave has waited for
-        // its own loads (one load group per slice is issued per iteration)
-        wait_vm<LOADS * (STAGES - 2)>();
-        __builtin_amdgcn_s_barrier();
-        // the buffer of slice kt-1 is free (every wave passed the barrier
-        // after reading it): it receives slice kt+STAGES-1 during compute
-        compute(ring + u * STAGE_BYTES, ring + ((u + STAGES - 1) % STAGES) * STAGE_BYTES, kt + STAGES - 1);
-      }
-    }
+  for (int s = 0; s < STAGES - 1; ++s) issue(s, s);
+  // one slice per iteration; stage su of slice kt is kt % STAGES (a rolling
+  // counter, so the accumulators never pass through a branch)
+  int su = 0;
+  for (int kt = 0; kt < KT; ++kt) {
+    // every wave's slice kt has landed once each wave has waited for its
+    // own loads (one load group per slice is issued per iteration)
+    wait_vm<LOADS * (STAGES - 2)>();
+    __builtin_amdgcn_s_barrier();
+    // the stage of slice kt-1 is free (every wave passed the barrier after
+    // reading it): it receives slice kt+STAGES-1 during this compute
+    const int nsu = su == 0 ? STAGES - 1 : su - 1;
+    compute(su, nsu, kt + STAGES - 1);
+    su = su == STAGES - 1 ? 0 : su + 1;
   }
   wait_vm<0>();  // no load may still target this workgroup's LDS
 

@@ -115,9 +115,10 @@ def round_to_bf16(a: np.ndarray) -> np.ndarray:
     NaN stays NaN; this is a storage conversion, nothing more.
     """
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    rounded = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
-    out = rounded.astype(np.uint32).view(np.float32)
+    u = a.view(np.uint32)
+    # no finite value or infinity carries out of 32 bits here
+    rounded = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) & np.uint32(0xFFFF0000)
+    out = rounded.view(np.float32)
     nan = np.isnan(a)
     if nan.any():
         out = out.copy()
