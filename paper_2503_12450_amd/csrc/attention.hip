@@ -3,7 +3,7 @@
 // is a query) and partial for the cached blocks (the N selected rows are the
 // queries, keys/values of every token come from the per-block cache).
 //
-// bf16 path: one workgroup per (slot, head, 64 queries); keys/values stream
+// bf16 path: one workgroup per (slot, head, 64 or 128 queries); keys/values stream
 // through LDS in blocks of 64 keys with an online softmax, so any sequence
 // length works.  The products are the transposed ones (S^T = K Q^T,
 // O^T = V^T P^T) so that every query stays in one MFMA column: a lane then
@@ -85,17 +85,18 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
   float l_run = 0.f;  // this lane's share of the row sum
 
   // A block is KB key rows of K (DH / 8 chunks of 16 bytes each) and DH rows
-  // of V^T (KB / 8 chunks each): DH / 16 chunks of each per thread.  The next
-  // block is loaded into registers while the current one is multiplied.
+  // of V^T (KB / 8 chunks each): 8 DH chunks of each, PER_T per thread.  The
+  // next block is loaded into registers while the current one is multiplied.
   constexpr int CH = DH / 8;
-  constexpr int PER_T = DH / 16;
-  static_assert(PER_T * THREADS == KB * CH && PER_T * THREADS == DH * (KB / 8), "block/threads");
+  constexpr int NCHUNK = KB * CH;
+  static_assert(NCHUNK == DH * (KB / 8), "block chunks");
+  constexpr int PER_T = (NCHUNK + THREADS - 1) / THREADS;
   const bool vec_v = (seq & 7) == 0;  // V^T rows 16-byte aligned
   u32x4_t rk[PER_T], rv[PER_T];
   auto load_block = [&](int key0) {
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) {
-      const int v = tid + THREADS * i;
+      const int v = min(tid + THREADS * i, NCHUNK - 1);  // a spare thread repeats the last chunk
       const int r = v / CH, c = v - (v / CH) * CH;
       const int key = key0 + r;
       rk[i] = key < seq ? *reinterpret_cast<const u32x4_t*>(kbase + static_cast<long>(key) * DH + 8 * c)
@@ -120,6 +121,7 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) {
       const int v = tid + THREADS * i;
+      if (NCHUNK % THREADS != 0 && v >= NCHUNK) break;
       const int r = v / CH, c = v - (v / CH) * CH;
       *reinterpret_cast<u32x4_t*>(Ks + r * KROW + 8 * c) = rk[i];
       const int d = v >> 3, c8 = v & 7;
@@ -277,18 +279,28 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
   for (int d = 0; d < DH; ++d) O[q_row * D + h * DH + d] = acc[d] * inv;
 }
 
+template <int DH, int WAVES>
+static void attn_bf16_launch(const void* q, const void* k, const void* v, void* out, int n_slots, int H,
+                             int seq, int per_slot, float scale_log2, hipStream_t st) {
+  const int qblocks = (per_slot + 32 * WAVES - 1) / (32 * WAVES);
+  const long grid = static_cast<long>(n_slots) * H * qblocks;
+  hipLaunchKernelGGL((attn_bf16_kernel<DH, WAVES>), dim3(static_cast<unsigned>(grid)), dim3(64 * WAVES), 0, st,
+                     static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k), static_cast<const bf16_t*>(v),
+                     static_cast<bf16_t*>(out), H, seq, per_slot, scale_log2);
+}
+
 template <int DH>
 static hipError_t attn_launch(int dtype, const void* q, const void* k, const void* v, void* out,
                               int n_slots, int H, int seq, int per_slot, hipStream_t st) {
   const float scale_log2 = kLog2e / sqrtf(static_cast<float>(DH));
   if (dtype == DT_BF16) {
-    constexpr int WAVES = 2;  // 64 queries per workgroup
-    const int qblocks = (per_slot + 32 * WAVES - 1) / (32 * WAVES);
-    const long grid = static_cast<long>(n_slots) * H * qblocks;
-    hipLaunchKernelGGL((attn_bf16_kernel<DH, WAVES>), dim3(static_cast<unsigned>(grid)), dim3(64 * WAVES), 0, st,
-                       static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
-                       static_cast<const bf16_t*>(v), static_cast<bf16_t*>(out), H, seq,
-                       per_slot, scale_log2);
+    // measured on MI355X: 128 queries per workgroup once there are more than
+    // 64 per slot (each slot's keys and values are then streamed fewer
+    // times), 64 for the partial launches of the cached blocks
+    if (per_slot > 64)
+      attn_bf16_launch<DH, 4>(q, k, v, out, n_slots, H, seq, per_slot, scale_log2, st);
+    else
+      attn_bf16_launch<DH, 2>(q, k, v, out, n_slots, H, seq, per_slot, scale_log2, st);
   } else {
     const int qblocks = (per_slot + 63) / 64;
     const long grid = static_cast<long>(n_slots) * H * qblocks;
