@@ -31,7 +31,7 @@ EXPORTED = (
     "mar_k_layernorm", "mar_k_linear", "mar_k_linear_residual", "mar_k_qkv",
     "mar_k_attention", "mar_k_scores", "mar_k_select", "mar_k_gemm_variant",
 )
-GEMM_VARIANTS = 6
+GEMM_VARIANTS = 12
 
 
 class MarError(RuntimeError):

@@ -23,7 +23,9 @@
 //
 // Epilogues (the block's elementwise work rides on the product):
 //   BIAS      out = C + b                     (storage dtype)
-//   GELU      out = gelu_erf(C + b)           (storage dtype)
+//   GELU      out = gelu(C + b)               (storage dtype; erf by
+//                                              Abramowitz & Stegun 7.1.26 in
+//                                              fp32, 7.1.27 for bf16 output)
 //   RESIDUAL  out[row'] = resid + C + b       (fp32; row' may scatter into
 //                                              the output cache, Eq. 9)
 //   QKV       q rows, and keys/values written straight into the per-block
@@ -31,6 +33,7 @@
 //             Keys are stored [slot, head, token, d]; values transposed,
 //             [slot, head, d, token], the layout the attention kernel's
 //             second product reads.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -74,6 +77,24 @@ __device__ __forceinline__ float gelu_erf(float x) {
   return x >= 0.0f ? x * (1.0f - q) : x * q;
 }
 
+// The same GELU for outputs stored in bf16, with erf from Abramowitz &
+// Stegun formula 7.1.27:
+//   erf(z) = 1 - 1 / (1 + a1 z + a2 z^2 + a3 z^3 + a4 z^4)^4,  z >= 0,
+//   |error| <= 5e-4,
+// so q = (1 - erf) / 2 = 0.5 / D^4: one reciprocal, no exponential.  The
+// error in gelu is at most 2.5e-4 |x|, a sixteenth of a bf16 rounding step.
+__device__ __forceinline__ float gelu_erf_bf16(float x) {
+  const float z = fabsf(x) * 0.70710678118654752440f;
+  float d = fmaf(0.078108f, z, 0.000972f);
+  d = fmaf(d, z, 0.230389f);
+  d = fmaf(d, z, 0.278393f);
+  d = fmaf(d, z, 1.0f);
+  const float r = __builtin_amdgcn_rcpf(d);
+  const float r2 = r * r;
+  const float xq = (0.5f * x) * (r2 * r2);  // x q
+  return x >= 0.0f ? x - xq : xq;
+}
+
 typedef __attribute__((ext_vector_type(4))) int i32x4_t;
 
 // Buffer descriptor over `bytes` bytes at `base` (raw, no stride).
@@ -96,12 +117,24 @@ __device__ __forceinline__ i32x4_t make_rsrc(const void* base, unsigned bytes) {
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(i32x4_t rsrc, unsigned lds_addr, int voff, int soff) {
+  // the descriptor is wave-uniform; readfirstlane keeps it in SGPRs even
+  // when it was picked by a select (a no-op when it is scalar already)
+  i32x4_t r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) r[i] = __builtin_amdgcn_readfirstlane(rsrc[i]);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
                :
-               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
+               : "s"(lds_addr), "v"(voff), "s"(r), "s"(soff)
                : "memory", "m0");
 }
 #pragma clang diagnostic pop
+
+// Workgroup barrier that waits for this wave's LDS operations only (a
+// __syncthreads would also drain the vector-memory counter, i.e. the loads
+// already in flight for later slices).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
 template <int N>
@@ -193,18 +226,26 @@ __device__ __forceinline__ int qkv_section(const EpiArgs& e, int ng) {
 // Epilogue of one 32-row strip of a wave's tile: rows m_strip + 0..31,
 // columns n_wave + 0..WN-1; sb is the bias of those columns (LDS), reg the
 // wave's LDS staging region (32 * WN * 4 bytes).
-template <typename T, int KIND, int WN>
+template <typename T, int KIND>
+using EpiOut = typename std::conditional<KIND == EPI_RESIDUAL, float, T>::type;  // output type
+
+// Rows r0 .. r0 + HS - 1 of the strip go through LDS in one pass (HS = 32,
+// or 16 when a 32-row region per wave does not fit the staging space); the
+// transposed value stores, which do not use LDS, are made in the pass r0 = 0.
+template <typename T, int KIND, int WN, int HS>
 __device__ __forceinline__ void epilogue_strip(const EpiArgs& e, const EpiCtx<T, KIND>& c, int M, int N,
                                                int m_strip, int n_wave, int lane, const float* sb,
-                                               const f32x16_t (&acc)[WN / 32], unsigned char* reg) {
+                                               const f32x16_t (&acc)[WN / 32], unsigned char* reg, int r0) {
   constexpr int TN = WN / 32;
-  typedef typename std::conditional<KIND == EPI_RESIDUAL, float, T>::type OT;  // output type
+  typedef EpiOut<T, KIND> OT;
   constexpr int OS = sizeof(OT);
   constexpr int RB = WN * OS;        // bytes per staged row
   constexpr int NCH = RB / 16;       // 16-byte chunks per row
   constexpr int COLS = 16 / OS;      // columns per chunk
-  static_assert((NCH & (NCH - 1)) == 0 && (32 * NCH) % 64 == 0, "chunks per staged row");
+  static_assert((NCH & (NCH - 1)) == 0 && (HS * NCH) % 64 == 0, "chunks per staged row");
   const int row = lane & 31, h4 = (lane >> 5) * 4;
+  const int lr = row - r0;  // staged row of this lane, when in [0, HS)
+  const bool in_pass = HS == 32 || static_cast<unsigned>(lr) < static_cast<unsigned>(HS);
 
   // 1. bias (+ activation) in registers, rows into LDS; chunk c of row r sits
   //    at chunk c ^ (r % NCH), which spreads a wave's accesses over the banks
@@ -218,18 +259,19 @@ __device__ __forceinline__ void epilogue_strip(const EpiArgs& e, const EpiCtx<T,
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         x[g][r] = acc[j][4 * g + r] + bv[r];
-        if constexpr (KIND == EPI_GELU) x[g][r] = gelu_erf(x[g][r]);
+        if constexpr (KIND == EPI_GELU) x[g][r] = sizeof(T) == 2 ? gelu_erf_bf16(x[g][r]) : gelu_erf(x[g][r]);
       }
       const int colb = (32 * j + 8 * g + h4) * OS;
-      lds_put4(reg + row * RB + ((((colb >> 4) ^ row) & (NCH - 1)) << 4) + (colb & 15), x[g],
-               static_cast<OT*>(nullptr));
+      if (in_pass)
+        lds_put4(reg + lr * RB + ((((colb >> 4) ^ lr) & (NCH - 1)) << 4) + (colb & 15), x[g],
+                 static_cast<OT*>(nullptr));
     }
     if constexpr (KIND == EPI_QKV) {
       // value columns: the transposed cache [slot, head, d, tok] takes one
       // element per store, straight from registers (lanes of consecutive
       // rows write consecutive tokens)
       const int ng0 = n_wave + 32 * j + e.n_offset;
-      if (qkv_section(e, ng0) == 2 && e.v_cache) {
+      if (r0 == 0 && qkv_section(e, ng0) == 2 && e.v_cache) {
         const int m = m_strip + row;
         const int mc = min(m, M - 1);
         const int slot = div_by(mc, e.slot_magic, e.slot_shift);
@@ -251,11 +293,11 @@ __device__ __forceinline__ void epilogue_strip(const EpiArgs& e, const EpiCtx<T,
 
   // 2. 16-byte chunks back out of LDS, eight lanes per 128 bytes of a row
 #pragma unroll
-  for (int it = 0; it < 32 * NCH / 64; ++it) {
+  for (int it = 0; it < HS * NCH / 64; ++it) {
     const int v = lane + 64 * it;
     const int r = v / NCH, ch = v & (NCH - 1);
     const u32x4_t val = *reinterpret_cast<const u32x4_t*>(reg + r * RB + (((ch ^ r) & (NCH - 1)) << 4));
-    const int m = m_strip + r;
+    const int m = m_strip + r0 + r;
     const int n = n_wave + ch * COLS;
     const bool ok = m < M && n < N;
     const int mc = min(m, M - 1);
@@ -313,7 +355,7 @@ __device__ __forceinline__ void tile_of(int b, int tiles_m, int tiles_n, int& tm
 // Within a row the 16-byte chunks are XOR-swizzled by (row / RPB) % NCH,
 // RPB = 256 / ROWB rows per 256 bytes of banks: the 16 lanes of one LDS
 // read phase (16 rows, one chunk each) then hit 16 distinct bank groups.
-template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int ROWB, int KIND>
+template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int ROWB, int KIND, bool PERSIST>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* __restrict__ A,
                                                                     const T* __restrict__ W, int M,
                                                                     int N, int K, EpiArgs e) {
@@ -337,29 +379,39 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   static_assert(STAGES >= 2 && STAGES <= 5, "stages");
 
   __shared__ __align__(1024) unsigned char ring[STAGES * STAGE_BYTES];
-  __shared__ __align__(16) float sbias[BN];
-  // epilogue staging: one region of 32 rows x WN fp32 per wave, in the ring
-  constexpr int REGION = 32 * WN * 4;
-  static_assert(NW * REGION <= STAGES * STAGE_BYTES, "epilogue staging fits the ring");
+  __shared__ __align__(16) float sbias[2][256];  // the bias of the current and the next tile
+  static_assert(BN <= 256, "bias slot");
+  // Epilogue staging, each wave in its own region of HS rows x WN outputs.
+  // One tile per workgroup: the whole ring, once its loads have drained.
+  // Persistent: the stage that held the tile's last slice, the one stage
+  // not receiving the next tile's first slices (A part first, then W part);
+  // HS drops to 16 rows when 32 do not fit.
+  typedef EpiOut<T, KIND> OT;
+  constexpr int OSZ = static_cast<int>(sizeof(OT));
+  constexpr int HS = !PERSIST || (A_BYTES / (32 * WN * OSZ)) + (B_BYTES / (32 * WN * OSZ)) >= NW ? 32 : 16;
+  constexpr int REGION = HS * WN * OSZ;
+  constexpr int REG_IN_A = PERSIST ? A_BYTES / REGION : NW;
+  static_assert(PERSIST ? REG_IN_A + B_BYTES / REGION >= NW : NW * REGION <= STAGES * STAGE_BYTES,
+                "epilogue staging space");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave - (wave / WAVES_N) * WAVES_N;
-  int tile_m, tile_n;
-  tile_of(blockIdx.x, (M + BM - 1) / BM, (N + BN - 1) / BN, tile_m, tile_n);
-  const int m_base = tile_m * BM;
-  const int n_base = tile_n * BN;
-
-  // the tile's bias, visible to the epilogue after the main loop's barriers
-  for (int t = tid; t < BN; t += 64 * NW) sbias[t] = e.bias[min(n_base + t, N - 1)];
-
+  const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+  const int total = tiles_m * tiles_n;
   const int Kb = K * static_cast<int>(sizeof(T));
-  const i32x4_t ra = make_rsrc(A + static_cast<long>(m_base) * K,
-                               static_cast<unsigned>(min(BM, M - m_base)) * Kb);
-  const i32x4_t rb = make_rsrc(W + static_cast<long>(n_base) * K,
-                               static_cast<unsigned>(min(BN, N - n_base)) * Kb);
   const int KT = Kb / ROWB;  // K * sizeof(T) is a multiple of 128
+
+  // operand descriptors of tile t (rows past M / N read as zeros)
+  auto tile_rsrc = [&](int t, i32x4_t& ra, i32x4_t& rb, i32x4_t& rbias) {
+    int tm, tn;
+    tile_of(t, tiles_m, tiles_n, tm, tn);
+    ra = make_rsrc(A + static_cast<long>(tm) * BM * K, static_cast<unsigned>(min(BM, M - tm * BM)) * Kb);
+    rb = make_rsrc(W + static_cast<long>(tn) * BN * K, static_cast<unsigned>(min(BN, N - tn * BN)) * Kb);
+    rbias = make_rsrc(e.bias + tn * BN, static_cast<unsigned>(min(BN, N - tn * BN)) * 4u);
+  };
+
   // A wave-wide load moves RPI rows (group grp) of one slice: lane -> row
   // grp*RPI + r_in, physical chunk pc.  The row's swizzle is
   // (4 grp + r_in / RPB) % NCH, so two lane offsets (even and odd groups)
@@ -370,14 +422,17 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   const int voff[2] = {r_in * Kb + ((pc ^ ((r_in / RPB) % NCH)) << 4),
                        r_in * Kb + ((pc ^ ((4 + r_in / RPB) % NCH)) << 4)};
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-  // Load q of a slice's LOADS wave-wide loads (A rows first, then W rows)
-  // into ring stage su.  Every operand but the lane offset is wave-uniform
-  // and computed from readfirstlane'd values, so it stays in SGPRs.
+  // Every operand of a load but the lane offset is wave-uniform and computed
+  // from readfirstlane'd values, so it stays in SGPRs.
   const unsigned lds_ring = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(
       static_cast<int>(reinterpret_cast<uintptr_t>(static_cast<unsigned char*>(ring)))));
+  const unsigned lds_bias = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(
+      static_cast<int>(reinterpret_cast<uintptr_t>(&sbias[0][0]))));
   const int Kb_u = __builtin_amdgcn_readfirstlane(Kb);
-  auto issue_one = [&](int su, int kt, int q) {
-    const int kb = kt < KT ? kt * ROWB : 0;  // past the end: a harmless reload of slice 0
+  // load q of slice ks (A rows first, then W rows) of the tile with
+  // descriptors (ra, rb) into ring stage su
+  auto issue_one = [&](i32x4_t ra, i32x4_t rb, int su, int ks, int q) {
+    const int kb = ks * ROWB;
     if (q < A_INSTR) {
       const int grp = wave_u * A_INSTR + q;
       dma16(ra, lds_ring + su * A_BYTES + grp * 1024, voff[q & 1], kb + grp * RPI * Kb_u);
@@ -387,18 +442,11 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
             kb + grp * RPI * Kb_u);
     }
   };
-  auto issue = [&](int su, int kt) {
-#pragma unroll
-    for (int q = 0; q < LOADS; ++q) issue_one(su, kt, q);
+  // the tile's bias (256 floats, zeros past N) into bias slot bs; one wave
+  // loads it, the others see it after the barrier that follows its wait
+  auto issue_bias = [&](i32x4_t rbias, int bs) {
+    if (wave_u == 0) dma16(rbias, lds_bias + bs * 1024, lane * 16, 0);
   };
-
-  f32x16_t acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   // fragment reads: lane -> row frow of a 32-row tile, 16-byte chunk
   // 2*kk + fch.  Tile rows start at multiples of 32, so the swizzle is
@@ -417,12 +465,14 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   auto frag_b = [&](int su, int j, int kk) {
     return *reinterpret_cast<const u32x4_t*>(ring + b_off[kk] + su * B_BYTES + j * 32 * ROWB);
   };
+
+  f32x16_t acc[TM][TN];
   // Fragments of k-step kk+1 are read while k-step kk multiplies, and the
-  // loads of slice kt_next into buffer nst are spread over the k-steps: a
-  // wave that issued all of them at once would queue behind every other
-  // wave's loads before reaching its first MFMA.
+  // loads of the slice STAGES-1 ahead are spread over the k-steps: a wave
+  // that issued all of them at once would queue behind every other wave's
+  // loads before reaching its first MFMA.
   constexpr int PER_STEP = (LOADS + KSTEPS - 1) / KSTEPS;
-  auto compute = [&](int su, int nsu, int kt_next) {
+  auto compute = [&](int su, i32x4_t la, i32x4_t lb, int lsu, int lks) {
     u32x4_t fa[2][TM], fb[2][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i) fa[0][i] = frag_a(su, i, 0);
@@ -438,7 +488,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
         for (int j = 0; j < TN; ++j) fb[cur ^ 1][j] = frag_b(su, j, kk + 1);
       }
 #pragma unroll
-      for (int q = kk * PER_STEP; q < (kk + 1) * PER_STEP && q < LOADS; ++q) issue_one(nsu, kt_next, q);
+      for (int q = kk * PER_STEP; q < (kk + 1) * PER_STEP && q < LOADS; ++q) issue_one(la, lb, lsu, lks, q);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -446,44 +496,131 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
     }
   };
 
+  const EpiCtx<T, KIND> ec = make_epi<T, KIND>(e, M, N);
+  // The ring streams slices without a break across this workgroup's tiles:
+  // while slice kt of a tile is multiplied, slice kt+STAGES-1 is loaded,
+  // which near the end of a tile is one of the first slices of the next.
+  // Past the last tile, a harmless reload of the current tile's slice 0
+  // keeps the number of loads per iteration fixed.
+  const int stride = PERSIST ? static_cast<int>(gridDim.x) : total;
+  int t = blockIdx.x;
+  if (KT < STAGES - 1) return;  // the launcher picks fewer stages for such a short K
+  i32x4_t ra, rb, rbias, na, nb, nbias;
+  tile_rsrc(t, ra, rb, rbias);
+  issue_bias(rbias, 0);
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s) issue(s, s);
-  // one slice per iteration; stage su of slice kt is kt % STAGES (a rolling
-  // counter, so the accumulators never pass through a branch)
-  int su = 0;
-  for (int kt = 0; kt < KT; ++kt) {
-    // every wave's slice kt has landed once each wave has waited for its
-    // own loads (one load group per slice is issued per iteration)
-    wait_vm<LOADS * (STAGES - 2)>();
-    __builtin_amdgcn_s_barrier();
-    // the stage of slice kt-1 is free (every wave passed the barrier after
-    // reading it): it receives slice kt+STAGES-1 during this compute
-    const int nsu = su == 0 ? STAGES - 1 : su - 1;
-    compute(su, nsu, kt + STAGES - 1);
-    su = su == STAGES - 1 ? 0 : su + 1;
+  for (int s = 0; s < STAGES - 1; ++s)
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) issue_one(ra, rb, s, s, q);
+  // stage su holds the slice being multiplied; bs the bias slot of tile t
+  int su = 0, bs = 0;
+  for (int it = 0; t < total; t += stride, ++it) {
+    const bool has_next = t + stride < total;
+    if (has_next) tile_rsrc(t + stride, na, nb, nbias);
+    int tm, tn;
+    tile_of(t, tiles_m, tiles_n, tm, tn);
+    const int m_base = tm * BM, n_base = tn * BN;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    for (int kt = 0; kt < KT; ++kt) {
+      // every wave's slice kt has landed once each wave has waited for its
+      // own loads (one load group per slice and iteration, plus at most one
+      // bias load, which only makes this wait stricter)
+      wait_vm<LOADS * (STAGES - 2)>();
+      __builtin_amdgcn_s_barrier();
+      // the stage of slice kt-1 is free (every wave passed the barrier after
+      // reading it): it receives slice kt+STAGES-1 during this compute
+      const int lsu = su == 0 ? STAGES - 1 : su - 1;
+      const int ahead = kt + STAGES - 1;
+      const bool nxt = ahead >= KT && has_next;  // that slice belongs to the next tile
+      if (nxt && ahead == KT) issue_bias(nbias, bs ^ 1);
+      // one call site: the accumulators never pass through a branch; the
+      // descriptors are picked component by component (scalar selects)
+      i32x4_t la, lb;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        la[c] = __builtin_amdgcn_readfirstlane(nxt ? na[c] : ra[c]);
+        lb[c] = __builtin_amdgcn_readfirstlane(nxt ? nb[c] : rb[c]);
+      }
+      compute(su, la, lb, lsu, ahead < KT ? ahead : (nxt ? ahead - KT : 0));
+      su = su == STAGES - 1 ? 0 : su + 1;
+    }
+    unsigned char* reg;
+    if constexpr (PERSIST) {
+      // the stage of the tile's last slice becomes this wave's staging space
+      lds_barrier();
+      const int fs = su == 0 ? STAGES - 1 : su - 1;
+      reg = wave < REG_IN_A ? ring + fs * A_BYTES + wave * REGION
+                            : ring + B_RING + fs * B_BYTES + (wave - REG_IN_A) * REGION;
+    } else {
+      wait_vm<0>();  // the reloads past the last slice still target the ring
+      lds_barrier();
+      reg = ring + wave * REGION;
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int r0 = 0; r0 < 32; r0 += HS) {
+        epilogue_strip<T, KIND, WN, HS>(e, ec, M, N, m_base + wm * WM + 32 * i, n_base + wn * WN, lane,
+                                        &sbias[bs][wn * WN], acc[i], reg, r0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    if (has_next) {
+      ra = na;
+      rb = nb;
+      bs ^= 1;
+    }
   }
   wait_vm<0>();  // no load may still target this workgroup's LDS
+}
 
-  __syncthreads();  // every wave is done with the ring: it becomes staging space
-
-  const EpiCtx<T, KIND> ec = make_epi<T, KIND>(e, M, N);
-  unsigned char* const reg = ring + wave * REGION;
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    epilogue_strip<T, KIND, WN>(e, ec, M, N, m_base + wm * WM + 32 * i, n_base + wn * WN, lane,
-                                sbias + wn * WN, acc[i], reg);
-    __builtin_amdgcn_sched_barrier(0);
+// Compute units of the current device (cached per device).
+static int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[dev] = n;
   }
+  return cus[dev];
+}
+
+// persist: launch only as many workgroups as fit on the device at once; each
+// loops over tiles (t, t + grid, ...) with its load ring streaming on across
+// tile boundaries.  Otherwise one workgroup per tile.
+template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int ROWB, int KIND, bool PERSIST>
+static hipError_t gemm_launch_as(const void* A, const void* W, int M, int N, int K, const EpiArgs& e,
+                                 hipStream_t st) {
+  auto kern = gemm_kernel<T, BM, BN, WAVES_M, WAVES_N, STAGES, ROWB, KIND, PERSIST>;
+  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  int grid = tiles;
+  if (PERSIST) {
+    static int per_cu = 0;
+    if (per_cu == 0) {
+      int n = 0;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, 64 * WAVES_M * WAVES_N, 0) != hipSuccess || n < 1)
+        n = 1;
+      per_cu = n;
+    }
+    grid = std::min(tiles, per_cu * device_cus());
+  }
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * WAVES_M * WAVES_N), 0, st, static_cast<const T*>(A),
+                     static_cast<const T*>(W), M, N, K, e);
+  return hipGetLastError();
 }
 
 template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int ROWB, int KIND>
-static hipError_t gemm_launch(const void* A, const void* W, int M, int N, int K,
-                              const EpiArgs& e, hipStream_t st) {
-  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WAVES_M, WAVES_N, STAGES, ROWB, KIND>), dim3(tiles),
-                     dim3(64 * WAVES_M * WAVES_N), 0, st, static_cast<const T*>(A),
-                     static_cast<const T*>(W), M, N, K, e);
-  return hipGetLastError();
+static hipError_t gemm_launch(const void* A, const void* W, int M, int N, int K, const EpiArgs& e,
+                              bool persist, hipStream_t st) {
+  return persist ? gemm_launch_as<T, BM, BN, WAVES_M, WAVES_N, STAGES, ROWB, KIND, true>(A, W, M, N, K, e, st)
+                 : gemm_launch_as<T, BM, BN, WAVES_M, WAVES_N, STAGES, ROWB, KIND, false>(A, W, M, N, K, e, st);
 }
 
 // Tile choice.  Every configuration uses the same MFMA and visits k in the
@@ -496,27 +633,36 @@ static hipError_t gemm_pick(const void* A, const void* W, int M, int N, int K, c
   int v = g_gemm_variant;
   if (v < 0) {
     // measured on MI355X over the block's shapes (d_model 1024, M from 3200
-    // to 40960): the fp32 residual products are epilogue-heavy and prefer
-    // 128-row tiles (128 x 256 once K is long and there are enough of
-    // them); the others take 256 x 256 tiles with a 4-deep ring of 64-byte
-    // slices, except in the middle range where two 128 x 128 workgroups
-    // per CU balance better
+    // to 40960): persistent launches win from a few hundred tiles on; the
+    // fp32 residual products are epilogue-heavy and prefer 128-row tiles
+    // (128 x 256, one tile per workgroup, once K is long and there are
+    // enough of them); the others
+    // take 256 x 256 tiles, with a 4-deep ring of 64-byte slices when there
+    // is at most one tile per CU and two 128 x 128 workgroups per CU in the
+    // middle range
     const long big = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
     const long small = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
     if (small <= 256)
       v = 1;
     else if (KIND == EPI_RESIDUAL)
-      v = (K >= 2048 && big >= 256) ? 3 : 4;
+      v = (K >= 2048 && big >= 256) ? 3 : 10;
     else
-      v = (big > 256 && big <= 512) ? 4 : 5;
+      v = big <= 256 ? 5 : (big <= 512 ? 10 : 6);
   }
+  // variants 6..11: the configurations of 0..5 launched persistent
+  const bool persist = v >= 6;
+  if (persist) v -= 6;
+  // a ring of S stages streams S-1 slices ahead within a tile: short K
+  // takes the two-stage configuration
+  static const int kStages[6] = {2, 3, 3, 3, 2, 4}, kRowB[6] = {128, 128, 128, 128, 128, 64};
+  if (K * static_cast<int>(sizeof(T)) / kRowB[v] < kStages[v] - 1) v = 4;
   switch (v) {
-    case 0: return gemm_launch<T, 256, 256, 2, 4, 2, 128, KIND>(A, W, M, N, K, e, st);
-    case 1: return gemm_launch<T, 128, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, st);
-    case 2: return gemm_launch<T, 256, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, st);
-    case 3: return gemm_launch<T, 128, 256, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, st);
-    case 5: return gemm_launch<T, 256, 256, 2, 4, 4, 64, KIND>(A, W, M, N, K, e, st);
-    default: return gemm_launch<T, 128, 128, 2, 2, 2, 128, KIND>(A, W, M, N, K, e, st);
+    case 0: return gemm_launch<T, 256, 256, 2, 4, 2, 128, KIND>(A, W, M, N, K, e, persist, st);
+    case 1: return gemm_launch<T, 128, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);
+    case 2: return gemm_launch<T, 256, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);
+    case 3: return gemm_launch<T, 128, 256, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);
+    case 5: return gemm_launch<T, 256, 256, 2, 4, 4, 64, KIND>(A, W, M, N, K, e, persist, st);
+    default: return gemm_launch<T, 128, 128, 2, 2, 2, 128, KIND>(A, W, M, N, K, e, persist, st);
   }
 }
 
