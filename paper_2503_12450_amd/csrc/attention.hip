@@ -3,7 +3,7 @@
 // is a query) and partial for the cached blocks (the N selected rows are the
 // queries, keys/values of every token come from the per-block cache).
 //
-// bf16 path: one workgroup per (slot, head, 64 or 128 queries); keys/values stream
+// bf16 path: one workgroup per (slot, head, 64 queries); keys/values stream
 // through LDS in blocks of 64 keys with an online softmax, so any sequence
 // length works.  The products are the transposed ones (S^T = K Q^T,
 // O^T = V^T P^T) so that every query stays in one MFMA column: a lane then
@@ -294,13 +294,9 @@ static hipError_t attn_launch(int dtype, const void* q, const void* k, const voi
                               int n_slots, int H, int seq, int per_slot, hipStream_t st) {
   const float scale_log2 = kLog2e / sqrtf(static_cast<float>(DH));
   if (dtype == DT_BF16) {
-    // measured on MI355X: 128 queries per workgroup once there are more than
-    // 64 per slot (each slot's keys and values are then streamed fewer
-    // times), 64 for the partial launches of the cached blocks
-    if (per_slot > 64)
-      attn_bf16_launch<DH, 4>(q, k, v, out, n_slots, H, seq, per_slot, scale_log2, st);
-    else
-      attn_bf16_launch<DH, 2>(q, k, v, out, n_slots, H, seq, per_slot, scale_log2, st);
+    // 64 queries per workgroup: 128 streams each slot's keys and values
+    // fewer times but measured no faster inside the MAR-L schedule
+    attn_bf16_launch<DH, 2>(q, k, v, out, n_slots, H, seq, per_slot, scale_log2, st);
   } else {
     const int qblocks = (per_slot + 63) / 64;
     const long grid = static_cast<long>(n_slots) * H * qblocks;

@@ -515,7 +515,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   // stage su holds the slice being multiplied; bs the bias slot of tile t
   int su = 0, bs = 0;
   for (int it = 0; t < total; t += stride, ++it) {
-    const bool has_next = t + stride < total;
+    const bool has_next = PERSIST && t + stride < total;
     if (has_next) tile_rsrc(t + stride, na, nb, nbias);
     int tm, tn;
     tile_of(t, tiles_m, tiles_n, tm, tn);
@@ -536,17 +536,21 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
       // reading it): it receives slice kt+STAGES-1 during this compute
       const int lsu = su == 0 ? STAGES - 1 : su - 1;
       const int ahead = kt + STAGES - 1;
-      const bool nxt = ahead >= KT && has_next;  // that slice belongs to the next tile
-      if (nxt && ahead == KT) issue_bias(nbias, bs ^ 1);
-      // one call site: the accumulators never pass through a branch; the
-      // descriptors are picked component by component (scalar selects)
-      i32x4_t la, lb;
+      if constexpr (PERSIST) {
+        const bool nxt = ahead >= KT && has_next;  // that slice belongs to the next tile
+        if (nxt && ahead == KT) issue_bias(nbias, bs ^ 1);
+        // one call site: the accumulators never pass through a branch; the
+        // descriptors are picked component by component (scalar selects)
+        i32x4_t la, lb;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        la[c] = __builtin_amdgcn_readfirstlane(nxt ? na[c] : ra[c]);
-        lb[c] = __builtin_amdgcn_readfirstlane(nxt ? nb[c] : rb[c]);
+        for (int c = 0; c < 4; ++c) {
+          la[c] = __builtin_amdgcn_readfirstlane(nxt ? na[c] : ra[c]);
+          lb[c] = __builtin_amdgcn_readfirstlane(nxt ? nb[c] : rb[c]);
+        }
+        compute(su, la, lb, lsu, ahead < KT ? ahead : (nxt ? ahead - KT : 0));
+      } else {
+        compute(su, ra, rb, lsu, ahead < KT ? ahead : 0);
       }
-      compute(su, la, lb, lsu, ahead < KT ? ahead : (nxt ? ahead - KT : 0));
       su = su == STAGES - 1 ? 0 : su + 1;
     }
     unsigned char* reg;
@@ -632,22 +636,27 @@ static hipError_t gemm_pick(const void* A, const void* W, int M, int N, int K, c
                             hipStream_t st) {
   int v = g_gemm_variant;
   if (v < 0) {
-    // measured on MI355X over the block's shapes (d_model 1024, M from 3200
-    // to 40960): persistent launches win from a few hundred tiles on; the
-    // fp32 residual products are epilogue-heavy and prefer 128-row tiles
-    // (128 x 256, one tile per workgroup, once K is long and there are
-    // enough of them); the others
-    // take 256 x 256 tiles, with a 4-deep ring of 64-byte slices when there
-    // is at most one tile per CU and two 128 x 128 workgroups per CU in the
-    // middle range
+    // measured on MI355X inside the 64-step MAR-L schedule (d_model 1024,
+    // M from 3200 to 40960; per-kernel times from same-box runs): the fp32
+    // residual products are epilogue-heavy and prefer 128-row tiles, one
+    // per workgroup (128 x 256 once K is long and there are enough of
+    // them); the others take 256 x 256 tiles with a 4-deep ring of 64-byte
+    // slices, except the GELU product at large M, which gains from a
+    // persistent launch (its long epilogue then overlaps the next tile's
+    // loads), and the middle range, where two 128 x 128 workgroups per CU
+    // balance better
     const long big = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
     const long small = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
     if (small <= 256)
       v = 1;
     else if (KIND == EPI_RESIDUAL)
-      v = (K >= 2048 && big >= 256) ? 3 : 10;
+      v = (K >= 2048 && big >= 256) ? 3 : 4;
+    else if (big <= 256)
+      v = 5;
+    else if (big <= 512)
+      v = KIND == EPI_GELU ? 10 : 4;
     else
-      v = big <= 256 ? 5 : (big <= 512 ? 10 : 6);
+      v = KIND == EPI_GELU ? 6 : 5;
   }
   // variants 6..11: the configurations of 0..5 launched persistent
   const bool persist = v >= 6;
