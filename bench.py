@@ -38,7 +38,77 @@ def parse():
                     help="kernel class timed with HIP events for the roofline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--decode-steps", type=int, default=64)
+    ap.add_argument("--fc1-shapes", action="store_true",
+                    help="only run the fc1 product once per shape the 64-step MAR-L schedule "
+                         "launches (for hardware-counter runs) and print each shape's launches per "
+                         "schedule")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy three times (the reference "
+                         "dispatch that scales the HBM byte counters) and exit")
     return ap.parse_args()
+
+
+COPY_BYTES = 1 << 30
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fc1_hbm_traffic_mar_l.md")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2503_12450_amd", "csrc", "gemm.hip")
+
+
+def calibrate_copy():
+    import torch
+    a = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda:0")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES, "dispatches": 3}), flush=True)
+
+
+def fc1_shapes(decode_steps: int):
+    """The fc1 products of one schedule: rows M -> launches.  Full steps run
+    every block on every row of both pathways; cached steps the prefix
+    blocks on every row and the rest on N rows per sequence."""
+    import torch
+
+    from paper_2503_12450_amd import binding as B
+    from paper_2503_12450_amd import schedule as sch
+    from paper_2503_12450_amd.workload import WORKLOADS
+
+    wl = WORKLOADS["mar-l"]
+    d, n, img = wl.dims, wl.n_recompute, wl.images
+    counts = {}
+    for p in sch.lazymar_schedule(decode_steps, 5, 9, "alternate"):
+        seqs = 2 * img if (p.mode == sch.FULL or p.branches == sch.BOTH) else img
+        if p.mode == sch.FULL:
+            counts[seqs * d.seq_len] = counts.get(seqs * d.seq_len, 0) + d.n_layers
+        else:
+            counts[seqs * d.seq_len] = counts.get(seqs * d.seq_len, 0) + d.full_prefix
+            counts[seqs * n] = counts.get(seqs * n, 0) + d.n_layers - d.full_prefix
+    g = torch.Generator(device="cuda:0").manual_seed(0)
+    w = (torch.randn(d.d_mlp, d.d_model, device="cuda:0", generator=g) * 0.02).to(torch.bfloat16)
+    bias = torch.zeros(d.d_mlp, device="cuda:0")
+    for m in sorted(counts, reverse=True):
+        a = torch.randn(m, d.d_model, device="cuda:0", generator=g).to(torch.bfloat16)
+        out = torch.empty(m, d.d_mlp, device="cuda:0", dtype=torch.bfloat16)
+        B.k_linear("bf16", a, w, bias, out, gelu=True)
+    torch.cuda.synchronize()
+    print(json.dumps({"fc1_rows_to_launches_per_schedule": counts, "n": d.d_mlp, "k": d.d_model}), flush=True)
+
+
+def recorded_traffic():
+    """HBM bytes per fc1 launch from the committed counter runs, or None when
+    the GEMM source changed since they were taken."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_FILE).read()
+        src = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    vals = dict(kv.split("=", 1) for kv in text.split() if kv.startswith(("traffic_bytes_per_launch=",
+                                                                           "gemm_source_sha256=")))
+    if vals.get("gemm_source_sha256") != src or "traffic_bytes_per_launch" not in vals:
+        return None
+    return float(vals["traffic_bytes_per_launch"])
 
 
 def cpu_baseline(dims, W, recipe, n, plans):
@@ -77,6 +147,12 @@ def cpu_baseline(dims, W, recipe, n, plans):
 
 def main():
     args = parse()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
+    if args.fc1_shapes:
+        fc1_shapes(args.decode_steps)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: the cached step shards over images with no "
@@ -168,7 +244,7 @@ def main():
         "kernel": f"{args.profile_kind} product (bf16 MFMA, fp32 accumulate)",
         "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
         "frac": (achieved / PEAK_BF16_TFLOPS) if achieved else None,
-        "traffic": None,
+        "traffic": recorded_traffic() if args.profile_kind == "fc1" and args.workload == "mar-l" else None,
         "launches": prof_n, "avg_launch_us": 1e3 * prof_ms / max(prof_n, 1),
         "flops_per_launch": prof_flops / max(prof_n, 1),
         "bytes_per_launch": prof_bytes / max(prof_n, 1),

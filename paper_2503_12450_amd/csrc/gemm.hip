@@ -606,13 +606,10 @@ static hipError_t gemm_launch_as(const void* A, const void* W, int M, int N, int
   const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
   int grid = tiles;
   if (PERSIST) {
-    static int per_cu = 0;
-    if (per_cu == 0) {
-      int n = 0;
-      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, 64 * WAVES_M * WAVES_N, 0) != hipSuccess || n < 1)
-        n = 1;
-      per_cu = n;
-    }
+    // resident workgroups per CU, limited by LDS (160 KiB per CU): the ring,
+    // the two bias slots and alignment slack; register use allows more
+    constexpr int kLds = STAGES * (BM + BN) * ROWB + 2 * 1024 + 1024;
+    constexpr int per_cu = kLds * 2 <= 160 * 1024 ? 2 : 1;
     grid = std::min(tiles, per_cu * device_cus());
   }
   hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * WAVES_M * WAVES_N), 0, st, static_cast<const T*>(A),
