@@ -122,16 +122,21 @@ def cpu_baseline(dims, W, recipe, n, plans):
     from paper_2503_12450_amd.workload import step_input
 
     threads = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()), default=1)
-    k = 20
-    prev = step_input(recipe, k - 1)[0]
-    x = step_input(recipe, k)[0]
+    # a bounded sample: REPS full and REPS cached steps of one sequence
+    # (decoding steps 20, 21, ...), the median of each
+    reps = 5
     orc = O.MarOracle(dims, W)
-    t0 = time.perf_counter()
-    orc.full_slot(0, prev)
-    t_full = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    orc.cached_slot(0, x, n)
-    t_cached = time.perf_counter() - t0
+    fulls, cacheds = [], []
+    for r in range(reps):
+        prev = step_input(recipe, 20 + 2 * r)[0]
+        x = step_input(recipe, 21 + 2 * r)[0]
+        t0 = time.perf_counter()
+        orc.full_slot(0, prev)
+        fulls.append(time.perf_counter() - t0)
+        t0 = time.perf_counter()
+        orc.cached_slot(0, x, n)
+        cacheds.append(time.perf_counter() - t0)
+    t_full, t_cached = float(np.median(fulls)), float(np.median(cacheds))
     full, cond, both = sch.counts(plans)
     seq_full = 2 * full
     seq_cached = 2 * both + cond
@@ -139,9 +144,9 @@ def cpu_baseline(dims, W, recipe, n, plans):
     tokens = len(plans) * dims.seq_len
     return {
         "value": tokens / t_sched, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-        "sample": (f"fp64 numpy oracle, one sequence: one full step ({t_full:.2f} s) and one token-cached "
-                   f"step N={n} ({t_cached:.2f} s) at the {dims.n_layers}-block width-{dims.d_model} shape; "
-                   f"one image's schedule composed as {seq_full} full + {seq_cached} cached sequence-steps"),
+        "sample": (f"fp64 numpy oracle, one sequence: median of {reps} full steps ({t_full:.2f} s) and of {reps} "
+                   f"token-cached steps N={n} ({t_cached:.2f} s) at the {dims.n_layers}-block width-{dims.d_model} "
+                   f"shape; one image's schedule composed as {seq_full} full + {seq_cached} cached sequence-steps"),
     }
 
 
