@@ -388,8 +388,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   // HS drops to 16 rows when 32 do not fit.
   typedef EpiOut<T, KIND> OT;
   constexpr int OSZ = static_cast<int>(sizeof(OT));
-  constexpr int HS = !PERSIST || (A_BYTES / (32 * WN * OSZ)) + (B_BYTES / (32 * WN * OSZ)) >= NW ? 32 : 16;
-  constexpr int REGION = HS * WN * OSZ;
+  constexpr int EC = WN < 64 ? WN : 64;  // columns per epilogue pass
+  constexpr int HS = !PERSIST || (A_BYTES / (32 * EC * OSZ)) + (B_BYTES / (32 * EC * OSZ)) >= NW ? 32 : 16;
+  constexpr int REGION = HS * EC * OSZ;
   constexpr int REG_IN_A = PERSIST ? A_BYTES / REGION : NW;
   static_assert(PERSIST ? REG_IN_A + B_BYTES / REGION >= NW : NW * REGION <= STAGES * STAGE_BYTES,
                 "epilogue staging space");
@@ -489,10 +490,15 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
       }
 #pragma unroll
       for (int q = kk * PER_STEP; q < (kk + 1) * PER_STEP && q < LOADS; ++q) issue_one(la, lb, lsu, lks, q);
+      // keep the reads of k-step kk+1 ahead of the MFMAs of k-step kk (left
+      // alone, the scheduler sinks each read next to its first use and the
+      // MFMAs wait on LDS latency at every k-step)
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) Mma<T>::run(acc[i][j], fb[cur][j], fa[cur][i]);  // C^T tile
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
@@ -565,13 +571,19 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
       lds_barrier();
       reg = ring + wave * REGION;
     }
+    // a pass covers EC columns (at most 64: 128-byte staged rows for bf16)
+    // so that only a few accumulator tiles are live at a time
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
-      for (int r0 = 0; r0 < 32; r0 += HS) {
-        epilogue_strip<T, KIND, WN, HS>(e, ec, M, N, m_base + wm * WM + 32 * i, n_base + wn * WN, lane,
-                                        &sbias[bs][wn * WN], acc[i], reg, r0);
-        __builtin_amdgcn_sched_barrier(0);
+      for (int j0 = 0; j0 < TN; j0 += EC / 32) {
+#pragma unroll
+        for (int r0 = 0; r0 < 32; r0 += HS) {
+          epilogue_strip<T, KIND, EC, HS>(e, ec, M, N, m_base + wm * WM + 32 * i, n_base + wn * WN + 32 * j0,
+                                          lane, &sbias[bs][wn * WN + 32 * j0],
+                                          *reinterpret_cast<const f32x16_t(*)[EC / 32]>(&acc[i][j0]), reg, r0);
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
     }
     if (has_next) {
@@ -633,27 +645,25 @@ static hipError_t gemm_pick(const void* A, const void* W, int M, int N, int K, c
                             hipStream_t st) {
   int v = g_gemm_variant;
   if (v < 0) {
-    // measured on MI355X inside the 64-step MAR-L schedule (d_model 1024,
-    // M from 3200 to 40960; per-kernel times from same-box runs): the fp32
-    // residual products are epilogue-heavy and prefer 128-row tiles, one
-    // per workgroup (128 x 256 once K is long and there are enough of
-    // them); the others take 256 x 256 tiles with a 4-deep ring of 64-byte
-    // slices, except the GELU product at large M, which gains from a
-    // persistent launch (its long epilogue then overlaps the next tile's
-    // loads), and the middle range, where two 128 x 128 workgroups per CU
-    // balance better
+    // measured on MI355X inside the MAR-L schedule (d_model 1024, M from
+    // 3200 to 40960): 256 x 256 tiles with a two-stage ring of 128-byte
+    // slices, launched persistent once there are several tiles per CU, and
+    // with a four-stage ring of 64-byte slices when there is about one tile
+    // per CU; 128 x 128 tiles (two workgroups per CU) for the fp32 residual
+    // products and the bias products in the middle range, where they
+    // balance better; a three-stage 128 x 128 ring for the fewest tiles
     const long big = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
     const long small = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
     if (small <= 256)
       v = 1;
     else if (KIND == EPI_RESIDUAL)
-      v = (K >= 2048 && big >= 256) ? 3 : 4;
+      v = big <= 512 ? 4 : 6;
     else if (big <= 256)
       v = 5;
     else if (big <= 512)
-      v = KIND == EPI_GELU ? 10 : 4;
+      v = KIND == EPI_GELU ? 0 : 4;
     else
-      v = KIND == EPI_GELU ? 6 : 5;
+      v = big <= 1280 ? 0 : 6;
   }
   // variants 6..11: the configurations of 0..5 launched persistent
   const bool persist = v >= 6;
