@@ -140,31 +140,61 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
     __syncthreads();
     if (kb + 1 < n_blocks) load_block(key0 + KB);
 
+    // All K fragments of the block first, then the S^T products, then the
+    // V^T fragments of the second product, so that their LDS latency hides
+    // under the softmax arithmetic (left alone, the scheduler sinks every
+    // read next to its MFMA and each MFMA waits on it).
+    u32x4_t kf[2][DS];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int st = 0; st < DS; ++st)
+        kf[sb][st] = *reinterpret_cast<const u32x4_t*>(Ks + (32 * sb + ql) * KROW + 16 * st + 8 * hg);
+    __builtin_amdgcn_sched_barrier(0);
     f32x16_t sc[2];
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) sc[sb][r] = 0.f;
 #pragma unroll
-      for (int st = 0; st < DS; ++st) {
-        const u32x4_t kf = *reinterpret_cast<const u32x4_t*>(Ks + (32 * sb + ql) * KROW + 16 * st + 8 * hg);
-        sc[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf),
+      for (int st = 0; st < DS; ++st)
+        sc[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf[sb][st]),
                                                          __builtin_bit_cast(bf16x8_t, qf[st]), sc[sb], 0, 0, 0);
-      }
     }
-    // scale, mask keys past the end, block max of this query over its two lanes
-    float tmax = -__builtin_huge_valf();
+    u32x4_t vfr[2][2][DT];  // keys 32 sb + 16 s2 + ..., rows 32 t + ql of V^T
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = key0 + 32 * sb + 8 * (r >> 2) + 4 * hg + (r & 3);
-        const float x = key < seq ? sc[sb][r] * scale_log2 : -__builtin_huge_valf();
-        sc[sb][r] = x;
-        tmax = fmaxf(tmax, x);
-      }
+      for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int t = 0; t < DT; ++t) {
+          const bf16_t* vr = Vt + (32 * t + ql) * VROW + 32 * sb + 16 * s2 + 4 * hg;
+          const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vr);
+          const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vr + 8);
+          vfr[sb][s2][t] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
+        }
+    __builtin_amdgcn_sched_barrier(0);
+    // block max of this query over its two lanes, on the unscaled scores
+    // (the scale is positive); keys past the end only in a partial block
+    float tmax = -__builtin_huge_valf();
+    if (key0 + KB <= seq) {
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sc[sb][r]);
+    } else {
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = key0 + 32 * sb + 8 * (r >> 2) + 4 * hg + (r & 3);
+          sc[sb][r] = key < seq ? sc[sb][r] : -__builtin_huge_valf();
+          tmax = fmaxf(tmax, sc[sb][r]);
+        }
+    }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float m_new = fmaxf(m_run, tmax);
+    // running max and exponents in log2 units: p = 2^(s * scale - m)
+    const float m_new = fmaxf(m_run, tmax * scale_log2);
     const float alpha = exp2f(m_run - m_new);
     m_run = m_new;
     float psum = 0.f;
@@ -172,7 +202,7 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(sc[sb][r] - m_new);
+        const float p = exp2f(fmaf(sc[sb][r], scale_log2, -m_new));
         sc[sb][r] = p;
         psum += p;
       }
@@ -193,11 +223,7 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
         pf[3] = pack2bf(sc[sb][8 * s2 + 6], sc[sb][8 * s2 + 7]);
 #pragma unroll
         for (int t = 0; t < DT; ++t) {
-          const bf16_t* vr = Vt + (32 * t + ql) * VROW + 32 * sb + 16 * s2 + 4 * hg;
-          const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vr);
-          const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vr + 8);
-          const u32x4_t vf = {lo[0], lo[1], hi[0], hi[1]};
-          oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vf),
+          oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vfr[sb][s2][t]),
                                                             __builtin_bit_cast(bf16x8_t, pf), oacc[t], 0, 0, 0);
         }
       }
