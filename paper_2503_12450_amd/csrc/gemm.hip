@@ -291,39 +291,69 @@ __device__ __forceinline__ void epilogue_strip(const EpiArgs& e, const EpiCtx<T,
     }
   }
 
-  // 2. 16-byte chunks back out of LDS, eight lanes per 128 bytes of a row
+  // 2. 16-byte chunks back out of LDS, eight lanes per 128 bytes of a row.
+  //    Every load of the pass (LDS chunks, residual rows, row indices) is
+  //    issued before any store: an output may alias the residual input, so
+  //    the compiler would otherwise keep each load behind the previous
+  //    chunk's store and pay a memory round trip per chunk.  Each element is
+  //    read before it is written, so the order is safe in place.
+  constexpr int IT = HS * NCH / 64;
+  u32x4_t val[IT];
+  int mrow[IT], ncol[IT];
 #pragma unroll
-  for (int it = 0; it < HS * NCH / 64; ++it) {
+  for (int it = 0; it < IT; ++it) {
     const int v = lane + 64 * it;
     const int r = v / NCH, ch = v & (NCH - 1);
-    const u32x4_t val = *reinterpret_cast<const u32x4_t*>(reg + r * RB + (((ch ^ r) & (NCH - 1)) << 4));
-    const int m = m_strip + r0 + r;
-    const int n = n_wave + ch * COLS;
-    const bool ok = m < M && n < N;
-    const int mc = min(m, M - 1);
-    if constexpr (KIND == EPI_BIAS || KIND == EPI_GELU) {
-      bstore16(c.out, ok ? (mc * N + n) * OS : kOob, val);
-    } else if constexpr (KIND == EPI_RESIDUAL) {
-      const int lin = ok ? (mc * N + n) * 4 : kOob;
-      const u32x4_t res = bload16(c.aux0, lin);
+    val[it] = *reinterpret_cast<const u32x4_t*>(reg + r * RB + (((ch ^ r) & (NCH - 1)) << 4));
+    mrow[it] = m_strip + r0 + r;
+    ncol[it] = n_wave + ch * COLS;
+  }
+  if constexpr (KIND == EPI_BIAS || KIND == EPI_GELU) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const bool ok = mrow[it] < M && ncol[it] < N;
+      bstore16(c.out, ok ? (mrow[it] * N + ncol[it]) * OS : kOob, val[it]);
+    }
+  } else if constexpr (KIND == EPI_RESIDUAL) {
+    u32x4_t res[IT];
+    int lin[IT], orow[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const bool ok = mrow[it] < M && ncol[it] < N;
+      const int mc = min(mrow[it], M - 1);
+      lin[it] = ok ? (mc * N + ncol[it]) * 4 : kOob;
+      res[it] = bload16(c.aux0, lin[it]);
+      orow[it] = e.out_idx ? div_by(mc, e.slot_magic, e.slot_shift) * e.seq + e.out_idx[mc] : mc;
+    }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
       u32x4_t y;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) y[q] = __float_as_uint(__uint_as_float(res[q]) + __uint_as_float(val[q]));
-      const int orow = e.out_idx ? div_by(mc, e.slot_magic, e.slot_shift) * e.seq + e.out_idx[mc] : mc;
-      bstore16(c.out, ok ? (orow * N + n) * 4 : kOob, y);
-      if (e.resid_copy) bstore16(c.aux1, lin, y);
-    } else {
-      const int ng = n + e.n_offset;
+      for (int q = 0; q < 4; ++q) y[q] = __float_as_uint(__uint_as_float(res[it][q]) + __uint_as_float(val[it][q]));
+      bstore16(c.out, lin[it] != kOob ? (orow[it] * N + ncol[it]) * 4 : kOob, y);
+      if (e.resid_copy) bstore16(c.aux1, lin[it], y);
+    }
+  } else {
+    int tok[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int mc = min(mrow[it], M - 1);
+      tok[it] = e.idx ? e.idx[mc] : mc - div_by(mc, e.slot_magic, e.slot_shift) * e.per_slot;
+    }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const bool ok = mrow[it] < M && ncol[it] < N;
+      const int mc = min(mrow[it], M - 1);
+      const int ng = ncol[it] + e.n_offset;
       const int sec = qkv_section(e, ng);
       const int rem = ng - sec * e.d_model;  // head * d_head + d
       const int slot = div_by(mc, e.slot_magic, e.slot_shift);
-      const int tok = e.idx ? e.idx[mc] : mc - slot * e.per_slot;
       const int head = div_by(rem, e.head_magic, e.head_shift);
       // [slot, head, tok, d]
-      const int krow = ((slot * e.n_heads + head) * e.seq + tok) * e.d_head + (rem - head * e.d_head);
-      bstore16(c.out, ok && sec == 0 ? (mc * e.d_model + rem) * OS : kOob, val);
-      bstore16(c.aux0, ok && sec == 1 ? krow * OS : kOob, val);
-      if (any_v && e.v_copy) bstore16(c.aux2, ok && sec == 2 ? krow * OS : kOob, val);
+      const int krow = ((slot * e.n_heads + head) * e.seq + tok[it]) * e.d_head + (rem - head * e.d_head);
+      bstore16(c.out, ok && sec == 0 ? (mc * e.d_model + rem) * OS : kOob, val[it]);
+      bstore16(c.aux0, ok && sec == 1 ? krow * OS : kOob, val[it]);
+      if (any_v && e.v_copy) bstore16(c.aux2, ok && sec == 2 ? krow * OS : kOob, val[it]);
     }
   }
 }
