@@ -499,10 +499,14 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
 
   f32x16_t acc[TM][TN];
   // Fragments of k-step kk+1 are read while k-step kk multiplies, and the
-  // loads of the slice STAGES-1 ahead are spread over the k-steps: a wave
-  // that issued all of them at once would queue behind every other wave's
-  // loads before reaching its first MFMA.
-  constexpr int PER_STEP = (LOADS + KSTEPS - 1) / KSTEPS;
+  // loads of the slice STAGES-1 ahead go out over the first two k-steps:
+  // issued all in the first, they queue behind every other wave's loads
+  // before the wave reaches its first MFMA; spread over every k-step, the
+  // last ones (in a two-stage ring) have a single k-step to land before the
+  // next slice's barrier (measured on MI355X inside the schedule: two
+  // k-steps beat one, three and four by 2-5 %).
+  constexpr int LOAD_STEPS = KSTEPS < 2 ? KSTEPS : 2;
+  constexpr int PER_STEP = (LOADS + LOAD_STEPS - 1) / LOAD_STEPS;
   auto compute = [&](int su, i32x4_t la, i32x4_t lb, int lsu, int lks) {
     u32x4_t fa[2][TM], fb[2][TN];
 #pragma unroll
