@@ -94,9 +94,19 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
   const bool vec_v = (seq & 7) == 0;  // V^T rows 16-byte aligned
   u32x4_t rk[PER_T], rv[PER_T];
   auto load_block = [&](int key0) {
+    if (vec_v && key0 + KB <= seq) {  // a whole block: no bounds to check
+#pragma unroll
+      for (int i = 0; i < PER_T; ++i) {
+        const int v = min(tid + THREADS * i, NCHUNK - 1);  // a spare thread repeats the last chunk
+        const int r = v / CH, c = v - (v / CH) * CH;
+        rk[i] = *reinterpret_cast<const u32x4_t*>(kbase + static_cast<long>(key0 + r) * DH + 8 * c);
+        rv[i] = *reinterpret_cast<const u32x4_t*>(vbase + static_cast<long>(v >> 3) * seq + key0 + 8 * (v & 7));
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) {
-      const int v = min(tid + THREADS * i, NCHUNK - 1);  // a spare thread repeats the last chunk
+      const int v = min(tid + THREADS * i, NCHUNK - 1);
       const int r = v / CH, c = v - (v / CH) * CH;
       const int key = key0 + r;
       rk[i] = key < seq ? *reinterpret_cast<const u32x4_t*>(kbase + static_cast<long>(key) * DH + 8 * c)
@@ -193,24 +203,34 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
         }
     }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    // running max and exponents in log2 units: p = 2^(s * scale - m)
-    const float m_new = fmaxf(m_run, tmax * scale_log2);
-    const float alpha = exp2f(m_run - m_new);
-    m_run = m_new;
+    // Exponents in log2 units against a reference m_run: p = 2^(s scale - m_run).
+    // The softmax is the same for any reference, so m_run only moves when
+    // some query of the wave sees a block maximum more than 2^8 above it
+    // (p then stays below 256, far inside the range of bf16 and fp32), and
+    // the rescale of the running sums is skipped for the other blocks.
+    const float m_blk = tmax * scale_log2;
+    if (__builtin_amdgcn_ballot_w64(m_blk > m_run + 8.f) != 0) {
+      const float m_new = fmaxf(m_run, m_blk);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first block
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[t][r] *= alpha;
+    }
+    // the hardware exp2 (no denormal handling: such p are far below what
+    // bf16 probabilities can hold next to the block's largest, which is >= 2^-8)
     float psum = 0.f;
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(fmaf(sc[sb][r], scale_log2, -m_new));
+        const float p = __builtin_amdgcn_exp2f(fmaf(sc[sb][r], scale_log2, -m_run));
         sc[sb][r] = p;
         psum += p;
       }
-    l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int t = 0; t < DT; ++t)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[t][r] *= alpha;
+    l_run += psum;
 
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb)

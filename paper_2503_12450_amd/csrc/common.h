@@ -55,8 +55,11 @@ __device__ __forceinline__ void unpack16(const u32x4_t& v, float* out, const bf1
   }
 }
 
+// Two fp32 -> two bf16 (round to nearest even) in one packed conversion.
+typedef __attribute__((ext_vector_type(2))) float f32x2_t;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
 __device__ __forceinline__ uint32_t pack2bf(float lo, float hi) {
-  return static_cast<uint32_t>(f2bf(lo)) | (static_cast<uint32_t>(f2bf(hi)) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 
 // Exact division by a divisor d >= 2 fixed for the launch (Granlund &
