@@ -498,16 +498,26 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   };
 
   f32x16_t acc[TM][TN];
-  // Fragments of k-step kk+1 are read while k-step kk multiplies, and the
-  // loads of the slice STAGES-1 ahead go out over the first two k-steps:
-  // issued all in the first, they queue behind every other wave's loads
-  // before the wave reaches its first MFMA; spread over every k-step, the
-  // last ones (in a two-stage ring) have a single k-step to land before the
-  // next slice's barrier (measured on MI355X inside the schedule: two
-  // k-steps beat one, three and four by 2-5 %).
+  // Early free (two-stage rings of four-wave workgroups): once every wave
+  // has read the last fragments of slice kt (a barrier after the reads of
+  // its last k-step), the stage receives slice kt+2 while that k-step
+  // multiplies, so the next barrier waits only for slice kt+1 and up to two
+  // slices are in flight.  The extra barrier per slice pays off where two
+  // workgroups share a CU (one multiplies while the other waits); with one
+  // eight-wave workgroup per CU it costs more than it gains (measured on
+  // MI355X: -5 % and +10-18 % per product).  Otherwise slice kt+STAGES-1 is
+  // loaded into the stage freed at the top of the iteration.
+  constexpr bool EF = STAGES == 2 && NW == 4;
+  constexpr int AHEAD = EF ? 2 : STAGES - 1;  // slices between the one multiplied and the one loaded
+  static_assert(!EF || KSTEPS >= 2, "early free needs two k-steps per slice");
+  // Fragments of k-step kk+1 are read while k-step kk multiplies.  Without
+  // early free, the loads of the slice STAGES-1 ahead go out over the first
+  // two k-steps: issued all in the first, they queue behind every other
+  // wave's loads before the wave reaches its first MFMA (measured on MI355X:
+  // two k-steps beat one, three and four by 2-5 %).
   constexpr int LOAD_STEPS = KSTEPS < 2 ? KSTEPS : 2;
   constexpr int PER_STEP = (LOADS + LOAD_STEPS - 1) / LOAD_STEPS;
-  auto compute = [&](int su, i32x4_t la, i32x4_t lb, int lsu, int lks) {
+  auto compute = [&](int su, i32x4_t la, i32x4_t lb, int lsu, int lks, bool do_load) {
     u32x4_t fa[2][TM], fb[2][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i) fa[0][i] = frag_a(su, i, 0);
@@ -522,34 +532,58 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
 #pragma unroll
         for (int j = 0; j < TN; ++j) fb[cur ^ 1][j] = frag_b(su, j, kk + 1);
       }
+      if constexpr (!EF) {
 #pragma unroll
-      for (int q = kk * PER_STEP; q < (kk + 1) * PER_STEP && q < LOADS; ++q) issue_one(la, lb, lsu, lks, q);
+        for (int q = kk * PER_STEP; q < (kk + 1) * PER_STEP && q < LOADS; ++q) issue_one(la, lb, lsu, lks, q);
+      }
       // keep the reads of k-step kk+1 ahead of the MFMAs of k-step kk (left
       // alone, the scheduler sinks each read next to its first use and the
       // MFMAs wait on LDS latency at every k-step)
       __builtin_amdgcn_sched_barrier(0);
+      // early free: the last k-step's MFMAs go out with the loads of slice
+      // kt+2 between them, so the matrix pipe starts before the loads queue
+      constexpr int LP = (LOADS + TM * TN - 1) / (TM * TN);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) Mma<T>::run(acc[i][j], fb[cur][j], fa[cur][i]);  // C^T tile
+        for (int j = 0; j < TN; ++j) {
+          Mma<T>::run(acc[i][j], fb[cur][j], fa[cur][i]);  // C^T tile
+          if constexpr (EF) {
+            if (kk == KSTEPS - 1 && do_load) {
+              __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+              for (int q = (i * TN + j) * LP; q < (i * TN + j + 1) * LP && q < LOADS; ++q)
+                issue_one(la, lb, lsu, lks, q);
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          }
+        }
       __builtin_amdgcn_sched_barrier(0);
+      if constexpr (EF) {
+        if (kk == KSTEPS - 2) {
+          lds_barrier();  // every wave has read its last fragments of stage su
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
     }
   };
 
   const EpiCtx<T, KIND> ec = make_epi<T, KIND>(e, M, N);
   // The ring streams slices without a break across this workgroup's tiles:
-  // while slice kt of a tile is multiplied, slice kt+STAGES-1 is loaded,
-  // which near the end of a tile is one of the first slices of the next.
-  // Past the last tile, a harmless reload of the current tile's slice 0
-  // keeps the number of loads per iteration fixed.
+  // while slice kt of a tile is multiplied, slice kt+AHEAD is loaded, which
+  // near the end of a tile is one of the first slices of the next.  With
+  // early free, the next tile's slice 1 waits for the epilogue (its stage is
+  // the staging space) and slices past the last tile are not loaded; deeper
+  // rings keep the number of loads per iteration fixed with a harmless
+  // reload of the current tile's slice 0.
   const int stride = PERSIST ? static_cast<int>(gridDim.x) : total;
   int t = blockIdx.x;
-  if (KT < STAGES - 1) return;  // the launcher picks fewer stages for such a short K
+  if (KT < (EF ? 2 : STAGES - 1)) return;  // the launcher picks another ring for such a short K
   i32x4_t ra, rb, rbias, na, nb, nbias;
   tile_rsrc(t, ra, rb, rbias);
   issue_bias(rbias, 0);
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
+  for (int s = 0; s < AHEAD; ++s)
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) issue_one(ra, rb, s, s, q);
   // stage su holds the slice being multiplied; bs the bias slot of tile t
@@ -568,40 +602,49 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     for (int kt = 0; kt < KT; ++kt) {
       // every wave's slice kt has landed once each wave has waited for its
-      // own loads (one load group per slice and iteration, plus at most one
-      // bias load, which only makes this wait stricter)
-      wait_vm<LOADS * (STAGES - 2)>();
+      // own loads of it: loads complete in issue order, so it waits until
+      // only the loads issued after them remain (one load group per slice,
+      // plus at most one bias load, which only makes the wait stricter)
+      if constexpr (EF) {
+        if (kt + 1 < KT || has_next) wait_vm<LOADS>();  // slice kt+1 was issued after slice kt
+        else wait_vm<0>();
+      } else {
+        wait_vm<LOADS * (STAGES - 2)>();
+      }
       __builtin_amdgcn_s_barrier();
-      // the stage of slice kt-1 is free (every wave passed the barrier after
-      // reading it): it receives slice kt+STAGES-1 during this compute
-      const int lsu = su == 0 ? STAGES - 1 : su - 1;
-      const int ahead = kt + STAGES - 1;
+      // without early free, the stage of slice kt-1 is free (every wave
+      // passed the barrier after reading it) and receives slice kt+STAGES-1;
+      // with early free, slice kt+2 goes into this slice's own stage
+      const int lsu = EF ? su : (su == 0 ? STAGES - 1 : su - 1);
+      const int ahead = kt + AHEAD;
       if constexpr (PERSIST) {
-        const bool nxt = ahead >= KT && has_next;  // that slice belongs to the next tile
-        if (nxt && ahead == KT) issue_bias(nbias, bs ^ 1);
+        const bool nxt = ahead >= KT;  // that slice belongs to the next tile
+        if (nxt && has_next && ahead == KT) issue_bias(nbias, bs ^ 1);
+        const bool do_load = EF ? ahead < KT || (has_next && ahead == KT) : true;
+        const bool use_next = nxt && has_next;
         // one call site: the accumulators never pass through a branch; the
         // descriptors are picked component by component (scalar selects)
         i32x4_t la, lb;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-          la[c] = __builtin_amdgcn_readfirstlane(nxt ? na[c] : ra[c]);
-          lb[c] = __builtin_amdgcn_readfirstlane(nxt ? nb[c] : rb[c]);
+          la[c] = __builtin_amdgcn_readfirstlane(use_next ? na[c] : ra[c]);
+          lb[c] = __builtin_amdgcn_readfirstlane(use_next ? nb[c] : rb[c]);
         }
-        compute(su, la, lb, lsu, ahead < KT ? ahead : (nxt ? ahead - KT : 0));
+        compute(su, la, lb, lsu, ahead < KT ? ahead : (use_next ? ahead - KT : 0), do_load);
       } else {
-        compute(su, ra, rb, lsu, ahead < KT ? ahead : 0);
+        compute(su, ra, rb, lsu, ahead < KT ? ahead : 0, !EF || ahead < KT);
       }
       su = su == STAGES - 1 ? 0 : su + 1;
     }
     unsigned char* reg;
+    const int fs = su == 0 ? STAGES - 1 : su - 1;  // the stage of the tile's last slice
     if constexpr (PERSIST) {
       // the stage of the tile's last slice becomes this wave's staging space
       lds_barrier();
-      const int fs = su == 0 ? STAGES - 1 : su - 1;
       reg = wave < REG_IN_A ? ring + fs * A_BYTES + wave * REGION
                             : ring + B_RING + fs * B_BYTES + (wave - REG_IN_A) * REGION;
     } else {
-      wait_vm<0>();  // the reloads past the last slice still target the ring
+      wait_vm<0>();  // no load may still target the ring
       lds_barrier();
       reg = ring + wave * REGION;
     }
@@ -621,6 +664,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
       }
     }
     if (has_next) {
+      if constexpr (EF) {
+        // the staging space is free again in every wave: the next tile's
+        // slice 1 goes into it
+        lds_barrier();
+#pragma unroll
+        for (int q = 0; q < LOADS; ++q) issue_one(na, nb, fs, 1, q);
+      }
       ra = na;
       rb = nb;
       bs ^= 1;
@@ -679,34 +729,34 @@ static hipError_t gemm_pick(const void* A, const void* W, int M, int N, int K, c
                             hipStream_t st) {
   int v = g_gemm_variant;
   if (v < 0) {
-    // measured on MI355X inside the MAR-L schedule (d_model 1024, M from
-    // 3200 to 40960): 256 x 256 tiles with a two-stage ring of 128-byte
-    // slices, launched persistent once there are several tiles per CU, and
-    // with a four-stage ring of 64-byte slices when there is about one tile
-    // per CU; 128 x 128 tiles (two workgroups per CU) for the fp32 residual
-    // products and the bias products in the middle range, where they
-    // balance better; a three-stage 128 x 128 ring for the fewest tiles
+    // measured on MI355X over the MAR-L schedule's shapes (d_model 1024, M
+    // from 3200 to 40960): 128 x 128 tiles with a three-stage ring when
+    // there are at most 256 of them; 128 x 128 tiles with two workgroups per
+    // CU (early free) for the fp32 residual products and the bias products
+    // in the middle range, where they balance better; otherwise 256 x 256
+    // tiles with a two-stage ring of 128-byte slices, launched persistent
+    // once there are several tiles per CU
     const long big = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
     const long small = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
     if (small <= 256)
       v = 1;
     else if (KIND == EPI_RESIDUAL)
       v = big <= 512 ? 4 : 6;
-    else if (big <= 256)
-      v = 5;
     else if (big <= 512)
-      v = KIND == EPI_GELU ? 0 : 4;
+      v = KIND == EPI_GELU || big <= 256 ? 0 : 4;
     else
       v = big <= 1280 ? 0 : 6;
   }
   // variants 6..11: the configurations of 0..5 launched persistent
   const bool persist = v >= 6;
   if (persist) v -= 6;
-  // a ring of S stages streams S-1 slices ahead within a tile: short K
-  // takes the two-stage configuration
-  static const int kStages[6] = {2, 3, 3, 3, 2, 4}, kRowB[6] = {128, 128, 128, 128, 128, 64};
-  if (K * static_cast<int>(sizeof(T)) / kRowB[v] < kStages[v] - 1) v = 4;
+  // a ring needs a minimum number of slices per tile (two for the two-stage
+  // rings, which load two slices ahead; S-1 for S stages): short K takes
+  // 128 x 128 tiles with 64-byte slices (K * sizeof(T) is a multiple of 128)
+  static const int kMinSlices[6] = {2, 2, 2, 2, 2, 3}, kRowB[6] = {128, 128, 128, 128, 128, 64};
+  if (K * static_cast<int>(sizeof(T)) / kRowB[v] < kMinSlices[v]) v = 6;
   switch (v) {
+    case 6: return gemm_launch<T, 128, 128, 2, 2, 2, 64, KIND>(A, W, M, N, K, e, persist, st);
     case 0: return gemm_launch<T, 256, 256, 2, 4, 2, 128, KIND>(A, W, M, N, K, e, persist, st);
     case 1: return gemm_launch<T, 128, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);
     case 2: return gemm_launch<T, 256, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);

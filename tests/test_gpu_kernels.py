@@ -126,6 +126,34 @@ def test_tile_variants_are_bitwise_identical(variant):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("variant", list(range(6, 12)))
+def test_persistent_workgroups_walk_several_tiles(dtype, variant):
+    """Persistent launches run one or two workgroups per CU; with 264 tiles
+    of 256 x 256 (1056 of 128 x 128) each workgroup carries its load ring
+    and bias across tile boundaries.  Same bits as one workgroup per tile,
+    and within tolerance of the oracle on sampled rows."""
+    M, N, K = 8448, 2048, 384
+    a_h = normal_rows((M, K), seed=95, dtype=dtype)
+    w_h = normal_rows((N, K), seed=96, std=0.05, dtype=dtype)
+    bias_h = normal_rows((N,), seed=97)
+    a, w, bias = to_device(a_h, dtype), to_device(w_h, dtype), to_device(bias_h, "f32")
+    ref = torch.empty((M, N), dtype=a.dtype, device=DEV)
+    out = torch.empty_like(ref)
+    try:
+        B.k_gemm_variant(variant - 6)
+        B.k_linear(dtype, a, w, bias, ref, gelu=True)
+        B.k_gemm_variant(variant)
+        B.k_linear(dtype, a, w, bias, out, gelu=True)
+    finally:
+        B.k_gemm_variant(-1)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
+    rows = np.array([0, 1, 255, 256, 4095, 4096, 8191, 8192, M - 1])
+    want = O.gelu(O.linear(a_h[rows], w_h, bias_h))
+    _close(out[torch.from_numpy(rows).to(DEV)], want, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_linear_residual_in_place_and_scatter(dtype):
     M, N, K = 200, 256, 512
     a = normal_rows((M, K), seed=31, dtype=dtype)
