@@ -11,9 +11,8 @@
  * Row mapping used below: with `idx` given, row m of a compact matrix belongs
  * to slot m / per_slot and token idx[m] of that slot; without it, row m is
  * token m % per_slot of slot m / per_slot (and per_slot must equal seq).
- * The key cache [slots, H, seq, d_head] holds one slot's keys of head h as a
- * contiguous seq x d_head block; the value cache [slots, H, d_head, seq]
- * holds the values transposed (one row per dimension, tokens along it).
+ * The key and value caches [slots, H, seq, d_head] hold one slot's keys (or
+ * values) of head h as a contiguous seq x d_head block.
  */
 #ifndef MAR_KERNELS_H
 #define MAR_KERNELS_H
@@ -60,9 +59,9 @@ mar_status mar_k_linear_residual(int32_t dtype, const void* a, const void* w, co
  * and bias pointing at column n_offset:
  *   query columns  -> q_out[m, c]                  ([m, D], dtype)
  *   key columns    -> k_cache[slot, head, tok, :]  ([slots, H, seq, dh])
- *   value columns  -> v_cache[slot, head, :, tok]  ([slots, H, dh, seq],
- *                     transposed; nullable) and v_copy[slot, head, tok, :]
- *                     ([slots, H, seq, dh]; nullable); one of them required
+ *   value columns  -> v_cache[slot, head, tok, :]  ([slots, H, seq, dh];
+ *                     nullable) and v_copy, a second buffer of the same
+ *                     layout (nullable); one of them required
  * slot/tok from the row mapping.  d_model % 64 == 0, d_head % 16 == 0,
  * n_offset % 32 == 0, n_cols % 8 == 0. */
 mar_status mar_k_qkv(int32_t dtype, const void* a, const void* w, const float* bias, int32_t m,
@@ -72,8 +71,8 @@ mar_status mar_k_qkv(int32_t dtype, const void* a, const void* w, const float* b
 
 /* Eq. (3) without mask for per_slot query rows per slot against all seq
  * keys of the slot: q, out [n_slots * per_slot, H * d_head] (head h at
- * columns h * d_head ...), k [n_slots, H, seq, d_head], v transposed
- * [n_slots, H, d_head, seq] (the value cache layout).  Scale
+ * columns h * d_head ...), k and v [n_slots, H, seq, d_head] (the cache
+ * layout).  Scale
  * 1/sqrt(d_head); softmax statistics in fp32.  d_head in {16, 32, ..., 128}.
  * per_slot == seq is the dense block; per_slot = N the cached one. */
 mar_status mar_k_attention(int32_t dtype, const void* q, const void* k, const void* v, void* out,

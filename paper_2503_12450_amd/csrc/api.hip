@@ -511,11 +511,13 @@ mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0, in
 
   if (mode == MAR_FULL) {
     for (int l = 0; l < c.L; ++l) {
-      // keys [slot, head, token, d]; values transposed for attention, and as
-      // token rows into the scoring reference at the scoring block
+      // keys and values [slot, head, token, d]: into the cache from block P
+      // on; the scoring block's values go to the scoring reference (as a
+      // second copy when that block is cached too)
       void* kd = l >= c.P ? offset<void>(cache->layers[l].kc, slot_off, c.es) : ktmp;
-      void* vd = l >= c.P ? offset<void>(cache->layers[l].vc, slot_off, c.es) : vtmp;
-      void* vcopy = l == score_layer ? vref : nullptr;
+      void* vd = l >= c.P ? offset<void>(cache->layers[l].vc, slot_off, c.es)
+                          : (l == score_layer ? vref : vtmp);
+      void* vcopy = l == score_layer && l >= c.P ? vref : nullptr;
       s = dense_block(c, l, l == 0, x, kd, vd, vcopy, l == c.L - 1 ? Yslot : nullptr);
       if (s != MAR_OK) return s;
     }
@@ -540,15 +542,15 @@ mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0, in
       e.d_head = c.dh;
       e.seq = S;
       e.per_slot = S;
-      e.v_cache = nullptr;  // value rows only, untransposed, for scoring
-      e.v_copy = vcur;
+      e.v_cache = vcur;  // value rows only, for scoring
+      e.v_copy = nullptr;
       const void* wv = offset<const void>(w.qkv_w, 2L * c.D * c.D, c.es);
       TIMED(MAR_PROF_QKV, 2.0 * Mfull * c.D * c.D,
             gemm_bytes(Mfull, c.D, c.D, static_cast<double>(c.es), static_cast<double>(c.es), false),
             launch_gemm(c.dtype, a, wv, Mfull, c.D, c.D, e, c.st), "value gemm");
     } else {
       for (int l = 0; l < c.P; ++l) {
-        s = dense_block(c, l, l == 0, x, ktmp, vtmp, l == score_layer ? vcur : nullptr, nullptr);
+        s = dense_block(c, l, l == 0, x, ktmp, l == score_layer ? vcur : vtmp, nullptr, nullptr);
         if (s != MAR_OK) return s;
       }
     }

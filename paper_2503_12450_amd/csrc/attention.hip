@@ -22,17 +22,34 @@ namespace marcache {
 constexpr int kKeyTile = 64;
 constexpr float kLog2e = 1.4426950408889634f;
 
-// bf16: WAVES waves of 32 queries per workgroup; keys and transposed values
-// (V^T, [d][key] per slot and head) stream through LDS in blocks of 64 keys.
+// bf16: WAVES waves of 32 queries per workgroup; keys and values (both
+// [key][d] per slot and head) stream through LDS in blocks of 64 keys.
 // Per block and wave, with 32x32x16 MFMAs:
 //   S^T (32 keys x 32 queries) = K Q^T   A = K rows from LDS, B = Q (registers)
-//   O^T (32 d x 32 queries)   += V^T P^T A = V^T rows from LDS, B = P (registers)
+//   O^T (32 d x 32 queries)   += V^T P^T A = V^T fragments, B = P (registers)
 // Lane (q, h) = (lane % 32, lane / 32) owns query q: S^T gives it keys
 // 8 j + 4 h + i (j, i = 0..3) of each 32-key half, which are exactly the
 // eight k-slots it feeds to the second product for each 16-key step (in a
 // permuted key order that the V^T operand follows), and O^T gives it rows
 // d = 8 j + 4 h + i of its query's output.  The softmax statistics of a
 // query live in its two lanes (q and q + 32).
+//
+// The V^T operand is read from the value rows with ds_read_b64_tr_b16: in
+// each group of 16 lanes, lane i receives element i % 4 of the 8 bytes
+// addressed by lane 4 s + i / 4, for s = 0..3.  When the group's lanes
+// address 4 key rows x 16 columns (lane j: key row j / 4, columns
+// 4 (j % 4) .. + 3), lane i therefore receives column i of 4 consecutive
+// keys: the 4 keys of one k-slot run of its V^T row.
+template <int DH>
+constexpr int value_row_stride() {
+  // padded d range of the O^T tiles, plus a row offset of 64 bytes modulo
+  // 256 so that the four key rows of a transposed read fall on different
+  // banks
+  int v = (DH + 31) / 32 * 32;
+  while ((v * 2) % 256 != 64 && (v * 2) % 256 != 192) v += 8;
+  return v;
+}
+
 template <int DH, int WAVES>
 __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __restrict__ Q,
                                                                const bf16_t* __restrict__ Kc,
@@ -42,13 +59,13 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
   constexpr int KB = 64;               // keys per LDS block
   constexpr int DS = DH / 16;          // k-steps of S^T
   constexpr int DT = (DH + 31) / 32;   // 32-row tiles of O^T
-  constexpr int DHP = DT * 32;         // V^T rows incl. zero padding
-  constexpr int KROW = DH + 8;         // K row stride (elements)
-  constexpr int VROW = KB + 4;         // V^T row stride: 136 bytes, conflict-free 8-byte reads
+  constexpr int DHP = DT * 32;         // O^T rows incl. padding
+  constexpr int KROW = DH + 8;         // key row stride (elements)
+  constexpr int VROW = value_row_stride<DH>();  // value row stride (elements), >= DHP
   constexpr int THREADS = 64 * WAVES;
   constexpr int QB = 32 * WAVES;
   __shared__ __align__(16) bf16_t Ks[KB * KROW];
-  __shared__ __align__(16) bf16_t Vt[DHP * VROW];
+  __shared__ __align__(16) bf16_t Vs[KB * VROW];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -71,11 +88,15 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
     qf[st] = q_ok ? *reinterpret_cast<const u32x4_t*>(Q + q_row * D + h * DH + 16 * st + 8 * hg)
                   : u32x4_t{0u, 0u, 0u, 0u};
   if constexpr (DHP > DH) {
-    for (int i = tid; i < (DHP - DH) * VROW; i += THREADS) Vt[DH * VROW + i] = 0;
+    // the d columns past DH feed only O^T rows that are never stored; they
+    // are zeroed once so that those rows stay finite
+    for (int i = tid; i < KB * (DHP - DH); i += THREADS)
+      Vs[(i / (DHP - DH)) * VROW + DH + i % (DHP - DH)] = 0;
   }
 
-  const bf16_t* kbase = Kc + (static_cast<long>(b) * H + h) * seq * DH;
-  const bf16_t* vbase = Vc + (static_cast<long>(b) * H + h) * seq * DH;  // [DH][seq]
+  const long head_off = (static_cast<long>(b) * H + h) * seq * DH;
+  const bf16_t* kbase = Kc + head_off;
+  const bf16_t* vbase = Vc + head_off;
   f32x16_t oacc[DT];
 #pragma unroll
   for (int t = 0; t < DT; ++t)
@@ -84,47 +105,31 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
   float m_run = -__builtin_huge_valf();
   float l_run = 0.f;  // this lane's share of the row sum
 
-  // A block is KB key rows of K (DH / 8 chunks of 16 bytes each) and DH rows
-  // of V^T (KB / 8 chunks each): 8 DH chunks of each, PER_T per thread.  The
-  // next block is loaded into registers while the current one is multiplied.
+  // A block is KB rows of keys and KB rows of values, DH / 8 chunks of 16
+  // bytes each, PER_T chunks of each per thread.  The next block is loaded
+  // into registers while the current one is multiplied.
   constexpr int CH = DH / 8;
   constexpr int NCHUNK = KB * CH;
-  static_assert(NCHUNK == DH * (KB / 8), "block chunks");
   constexpr int PER_T = (NCHUNK + THREADS - 1) / THREADS;
-  const bool vec_v = (seq & 7) == 0;  // V^T rows 16-byte aligned
   u32x4_t rk[PER_T], rv[PER_T];
   auto load_block = [&](int key0) {
-    if (vec_v && key0 + KB <= seq) {  // a whole block: no bounds to check
+    if (key0 + KB <= seq) {  // a whole block: no bounds to check
 #pragma unroll
       for (int i = 0; i < PER_T; ++i) {
         const int v = min(tid + THREADS * i, NCHUNK - 1);  // a spare thread repeats the last chunk
-        const int r = v / CH, c = v - (v / CH) * CH;
-        rk[i] = *reinterpret_cast<const u32x4_t*>(kbase + static_cast<long>(key0 + r) * DH + 8 * c);
-        rv[i] = *reinterpret_cast<const u32x4_t*>(vbase + static_cast<long>(v >> 3) * seq + key0 + 8 * (v & 7));
+        const long off = static_cast<long>(key0 + v / CH) * DH + 8 * (v % CH);
+        rk[i] = *reinterpret_cast<const u32x4_t*>(kbase + off);
+        rv[i] = *reinterpret_cast<const u32x4_t*>(vbase + off);
       }
       return;
     }
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) {
       const int v = min(tid + THREADS * i, NCHUNK - 1);
-      const int r = v / CH, c = v - (v / CH) * CH;
-      const int key = key0 + r;
-      rk[i] = key < seq ? *reinterpret_cast<const u32x4_t*>(kbase + static_cast<long>(key) * DH + 8 * c)
-                        : u32x4_t{0u, 0u, 0u, 0u};
-      const int d = v >> 3, k8 = key0 + 8 * (v & 7);
-      const bf16_t* src = vbase + static_cast<long>(d) * seq + k8;
-      if (vec_v && k8 + 8 <= seq) {
-        rv[i] = *reinterpret_cast<const u32x4_t*>(src);
-      } else {
-        uint32_t w[4];
-#pragma unroll
-        for (int e2 = 0; e2 < 4; ++e2) {
-          const uint32_t lo = k8 + 2 * e2 < seq ? src[2 * e2] : 0u;
-          const uint32_t hi = k8 + 2 * e2 + 1 < seq ? src[2 * e2 + 1] : 0u;
-          w[e2] = lo | (hi << 16);
-        }
-        rv[i] = u32x4_t{w[0], w[1], w[2], w[3]};
-      }
+      const int key = key0 + v / CH;
+      const long off = static_cast<long>(key) * DH + 8 * (v % CH);
+      rk[i] = key < seq ? *reinterpret_cast<const u32x4_t*>(kbase + off) : u32x4_t{0u, 0u, 0u, 0u};
+      rv[i] = key < seq ? *reinterpret_cast<const u32x4_t*>(vbase + off) : u32x4_t{0u, 0u, 0u, 0u};
     }
   };
   auto store_block = [&]() {
@@ -134,11 +139,17 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
       if (NCHUNK % THREADS != 0 && v >= NCHUNK) break;
       const int r = v / CH, c = v - (v / CH) * CH;
       *reinterpret_cast<u32x4_t*>(Ks + r * KROW + 8 * c) = rk[i];
-      const int d = v >> 3, c8 = v & 7;
-      u32x2_t* dst = reinterpret_cast<u32x2_t*>(Vt + d * VROW + 8 * c8);
-      dst[0] = u32x2_t{rv[i][0], rv[i][1]};
-      dst[1] = u32x2_t{rv[i][2], rv[i][3]};
+      *reinterpret_cast<u32x4_t*>(Vs + r * VROW + 8 * c) = rv[i];
     }
+  };
+  // transposed reads: key row and d column this lane addresses
+  const int tr_row = (lane & 15) >> 2;
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  typedef __attribute__((ext_vector_type(4))) short s16x4_t;
+  auto read_tr = [](const bf16_t* p) {
+    const s16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4_t*)(p));
+    return __builtin_bit_cast(u32x2_t, v);
   };
 
   const int n_blocks = (seq + KB - 1) / KB;
@@ -178,9 +189,9 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
       for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
         for (int t = 0; t < DT; ++t) {
-          const bf16_t* vr = Vt + (32 * t + ql) * VROW + 32 * sb + 16 * s2 + 4 * hg;
-          const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vr);
-          const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vr + 8);
+          const bf16_t* vr = Vs + (32 * sb + 16 * s2 + 4 * hg + tr_row) * VROW + 32 * t + tr_col;
+          const u32x2_t lo = read_tr(vr);             // keys 4 hg + 0..3 of the 16-key step
+          const u32x2_t hi = read_tr(vr + 8 * VROW);  // keys 8 + 4 hg + 0..3
           vfr[sb][s2][t] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
         }
     __builtin_amdgcn_sched_barrier(0);
@@ -267,8 +278,8 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
     }
 }
 
-// fp32: 64 queries per workgroup, one per lane; keys and transposed values
-// tiled in LDS.
+// fp32: 64 queries per workgroup, one per lane; keys and values (the
+// values transposed on the way in) tiled in LDS.
 template <int DH>
 __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ Q,
                                                       const float* __restrict__ Kc,
@@ -294,7 +305,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
     acc[d] = 0.f;
   }
   const float* kbase = Kc + (static_cast<long>(b) * H + h) * seq * DH;
-  const float* vbase = Vc + (static_cast<long>(b) * H + h) * seq * DH;  // [DH][seq]
+  const float* vbase = Vc + (static_cast<long>(b) * H + h) * seq * DH;  // [seq][DH]
   float m_run = -__builtin_huge_valf(), l_run = 0.f;
   for (int key0 = 0; key0 < seq; key0 += kKeyTile) {
     const int nk = min(kKeyTile, seq - key0);
@@ -302,7 +313,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
     for (int e = lane; e < nk * DH; e += 64) Ks[e] = kbase[static_cast<long>(key0) * DH + e];
     for (int e = lane; e < DH * kKeyTile; e += 64) {
       const int d = e / kKeyTile, j = e - d * kKeyTile;
-      Vt[e] = j < nk ? vbase[static_cast<long>(d) * seq + key0 + j] : 0.f;
+      Vt[e] = j < nk ? vbase[static_cast<long>(key0 + j) * DH + d] : 0.f;
     }
     __syncthreads();
     for (int j = 0; j < nk; ++j) {

@@ -130,8 +130,8 @@ struct EpiArgs {
   const int32_t* out_idx;
   float* resid_copy;
   // QKV: n_global = n + n_offset selects q (< D), k (< 2D) or v; keys go to
-  // k_cache[slot][head][tok][d], values to v_cache[slot][head][d][tok]
-  // (transposed), with slot/tok from the row mapping (idx or dense).
+  // k_cache[slot][head][tok][d], values to v_cache[slot][head][tok][d] (and
+  // v_copy, same layout), with slot/tok from the row mapping (idx or dense).
   int n_offset;
   int d_model, n_heads, d_head, seq, per_slot;
   // m / per_slot = umulhi(m, slot_magic) >> slot_shift (set by launch_gemm)
@@ -143,7 +143,7 @@ struct EpiArgs {
   const int32_t* idx;
   void* k_cache;
   void* v_cache;
-  void* v_copy;  // nullable: value rows again, untransposed [slot][head][tok][d]
+  void* v_copy;  // nullable: value rows again, [slot][head][tok][d]
 };
 
 hipError_t launch_gemm(int dtype, const void* A, const void* W, int M, int N, int K,
@@ -151,8 +151,8 @@ hipError_t launch_gemm(int dtype, const void* A, const void* W, int M, int N, in
 void set_gemm_variant(int v);  // -1: by shape
 
 // Attention of per_slot queries per slot against the seq keys of the slot:
-// q, out [n_slots * per_slot, D] (head h at columns h*dh..); k
-// [n_slots, H, seq, dh]; v transposed, [n_slots, H, dh, seq].
+// q, out [n_slots * per_slot, D] (head h at columns h*dh..); k and v
+// [n_slots, H, seq, dh].
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v, void* out,
                             int n_slots, int H, int seq, int dh, int per_slot,
                             hipStream_t st);

@@ -30,9 +30,8 @@
 //                                              the output cache, Eq. 9)
 //   QKV       q rows, and keys/values written straight into the per-block
 //             cache at the row's (slot, token): the cache update of Eq. 9.
-//             Keys are stored [slot, head, token, d]; values transposed,
-//             [slot, head, d, token], the layout the attention kernel's
-//             second product reads.
+//             Keys and values are both stored [slot, head, token, d]
+//             (whole 16-byte row chunks, also for scattered tokens).
 #include <algorithm>
 #include <type_traits>
 
@@ -230,8 +229,7 @@ template <typename T, int KIND>
 using EpiOut = typename std::conditional<KIND == EPI_RESIDUAL, float, T>::type;  // output type
 
 // Rows r0 .. r0 + HS - 1 of the strip go through LDS in one pass (HS = 32,
-// or 16 when a 32-row region per wave does not fit the staging space); the
-// transposed value stores, which do not use LDS, are made in the pass r0 = 0.
+// or 16 when a 32-row region per wave does not fit the staging space).
 template <typename T, int KIND, int WN, int HS>
 __device__ __forceinline__ void epilogue_strip(const EpiArgs& e, const EpiCtx<T, KIND>& c, int M, int N,
                                                int m_strip, int n_wave, int lane, const float* sb,
@@ -249,7 +247,6 @@ __device__ __forceinline__ void epilogue_strip(const EpiArgs& e, const EpiCtx<T,
 
   // 1. bias (+ activation) in registers, rows into LDS; chunk c of row r sits
   //    at chunk c ^ (r % NCH), which spreads a wave's accesses over the banks
-  bool any_v = false;
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     float x[4][4];
@@ -265,29 +262,6 @@ __device__ __forceinline__ void epilogue_strip(const EpiArgs& e, const EpiCtx<T,
       if (in_pass)
         lds_put4(reg + lr * RB + ((((colb >> 4) ^ lr) & (NCH - 1)) << 4) + (colb & 15), x[g],
                  static_cast<OT*>(nullptr));
-    }
-    if constexpr (KIND == EPI_QKV) {
-      // value columns: the transposed cache [slot, head, d, tok] takes one
-      // element per store, straight from registers (lanes of consecutive
-      // rows write consecutive tokens)
-      const int ng0 = n_wave + 32 * j + e.n_offset;
-      if (r0 == 0 && qkv_section(e, ng0) == 2 && e.v_cache) {
-        const int m = m_strip + row;
-        const int mc = min(m, M - 1);
-        const int slot = div_by(mc, e.slot_magic, e.slot_shift);
-        const int tok = e.idx ? e.idx[mc] : mc - slot * e.per_slot;
-        const int vrow = slot * e.n_heads * e.d_head * e.seq + tok;
-        const int rem0 = ng0 - 2 * e.d_model;
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const bool ok = m < M && n_wave + 32 * j + 8 * g + h4 < N;
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            bstore1(c.aux1, ok ? (vrow + (rem0 + 8 * g + h4 + r) * e.seq) * OS : kOob, x[g][r],
-                    static_cast<OT*>(nullptr));
-        }
-      }
-      any_v = any_v || qkv_section(e, ng0) == 2;
     }
   }
 
@@ -353,7 +327,8 @@ __device__ __forceinline__ void epilogue_strip(const EpiArgs& e, const EpiCtx<T,
       const int krow = ((slot * e.n_heads + head) * e.seq + tok[it]) * e.d_head + (rem - head * e.d_head);
       bstore16(c.out, ok && sec == 0 ? (mc * e.d_model + rem) * OS : kOob, val[it]);
       bstore16(c.aux0, ok && sec == 1 ? krow * OS : kOob, val[it]);
-      if (any_v && e.v_copy) bstore16(c.aux2, ok && sec == 2 ? krow * OS : kOob, val[it]);
+      bstore16(c.aux1, ok && sec == 2 ? krow * OS : kOob, val[it]);
+      if (e.v_copy) bstore16(c.aux2, ok && sec == 2 ? krow * OS : kOob, val[it]);
     }
   }
 }

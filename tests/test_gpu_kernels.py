@@ -197,23 +197,23 @@ def test_qkv_dense_and_scattered(dtype, D, H):
     td = to_device(a[:1], dtype).dtype
     q = torch.empty((M, D), dtype=td, device=DEV)
     kc = torch.zeros((slots, H, S, dh), dtype=td, device=DEV)
-    vc = torch.zeros((slots, H, dh, S), dtype=td, device=DEV)       # transposed value cache
+    vc = torch.zeros((slots, H, S, dh), dtype=td, device=DEV)
     vcopy = torch.zeros((slots, H, S, dh), dtype=td, device=DEV)
     B.k_qkv(dtype, to_device(a, dtype), to_device(w, dtype), to_device(bias, "f32"), D, H, S, S,
             q_out=q, k_cache=kc, v_cache=vc, v_copy=vcopy)
     torch.cuda.synchronize()
     _close(q, ref[:, :D], dtype)
     _close(kc, _cache_layout(ref[:, D:2 * D].reshape(slots, S, D), H), dtype)
-    # values: the cache is transposed [slot, head, d, token], the copy is not
-    _close(vc, _cache_layout(ref[:, 2 * D:].reshape(slots, S, D), H).transpose(0, 1, 3, 2), dtype)
-    np.testing.assert_array_equal(_host(vcopy), _host(vc).transpose(0, 1, 3, 2))
+    # values: the cache and the copy share the key layout [slot, head, token, d]
+    _close(vc, _cache_layout(ref[:, 2 * D:].reshape(slots, S, D), H), dtype)
+    np.testing.assert_array_equal(_host(vcopy), _host(vc))
     # compact rows: keys/values land at their tokens, other rows untouched
     N = 9
     idx = random_index_sets(slots, S, N, seed=44)
     ac = normal_rows((slots * N, D), seed=45, dtype=dtype)
     refc = O.linear(ac, w, bias)
     kc2 = torch.full((slots, H, S, dh), 5.0, dtype=td, device=DEV)
-    vc2 = torch.full((slots, H, dh, S), 5.0, dtype=td, device=DEV)
+    vc2 = torch.full((slots, H, S, dh), 5.0, dtype=td, device=DEV)
     qc = torch.empty((slots * N, D), dtype=td, device=DEV)
     B.k_qkv(dtype, to_device(ac, dtype), to_device(w, dtype), to_device(bias, "f32"), D, H, S, N,
             q_out=qc, k_cache=kc2, v_cache=vc2, idx=torch.from_numpy(idx.reshape(-1)).to(DEV))
@@ -223,11 +223,11 @@ def test_qkv_dense_and_scattered(dtype, D, H):
     for s in range(slots):
         rows = refc[s * N:(s + 1) * N]
         _close(k2[s][:, idx[s]], rows[:, D:2 * D].reshape(N, H, dh).transpose(1, 0, 2), dtype)
-        _close(v2[s][:, :, idx[s]], rows[:, 2 * D:].reshape(N, H, dh).transpose(1, 2, 0), dtype)
+        _close(v2[s][:, idx[s]], rows[:, 2 * D:].reshape(N, H, dh).transpose(1, 0, 2), dtype)
         other = np.setdiff1d(np.arange(S), idx[s])
-        assert np.all(k2[s][:, other] == 5.0) and np.all(v2[s][:, :, other] == 5.0)
+        assert np.all(k2[s][:, other] == 5.0) and np.all(v2[s][:, other] == 5.0)
     # value columns only (the scoring pass when no block is always computed)
-    vonly = torch.zeros((slots, H, dh, S), dtype=td, device=DEV)
+    vonly = torch.zeros((slots, H, S, dh), dtype=td, device=DEV)
     wd = to_device(w, dtype)
     bd = to_device(bias, "f32")
     B.k_qkv(dtype, to_device(a, dtype), wd[2 * D:], bd[2 * D:], D, H, S, S, v_cache=vonly,
@@ -252,8 +252,7 @@ def test_attention(dtype, S, dh, H, per):
     v = normal_rows((slots, H, S, dh), seed=53, dtype=dtype)
     td = to_device(q[:1], dtype).dtype
     out = torch.empty((slots * per, D), dtype=td, device=DEV)
-    vt = np.ascontiguousarray(v.transpose(0, 1, 3, 2))   # the value cache is transposed
-    B.k_attention(dtype, to_device(q, dtype), to_device(k, dtype), to_device(vt, dtype), out, slots, H, S, dh, per)
+    B.k_attention(dtype, to_device(q, dtype), to_device(k, dtype), to_device(v, dtype), out, slots, H, S, dh, per)
     torch.cuda.synchronize()
     ref = np.empty((slots * per, D))
     for s in range(slots):
@@ -272,7 +271,7 @@ def test_attention_query_rows_independent(dtype):
     q = normal_rows((slots * S, D), seed=54, dtype=dtype)
     k = normal_rows((slots, H, S, dh), seed=55, dtype=dtype)
     v = normal_rows((slots, H, S, dh), seed=56, dtype=dtype)
-    kd, vd = to_device(k, dtype), to_device(np.ascontiguousarray(v.transpose(0, 1, 3, 2)), dtype)
+    kd, vd = to_device(k, dtype), to_device(v, dtype)
     td = kd.dtype
     dense = torch.empty((slots * S, D), dtype=td, device=DEV)
     B.k_attention(dtype, to_device(q, dtype), kd, vd, dense, slots, H, S, dh, S)
