@@ -215,15 +215,17 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bf16_kernel(const bf16_t* __r
     }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
     // Exponents in log2 units against a reference m_run: p = 2^(s scale - m_run).
-    // The softmax is the same for any reference, so m_run only moves when
-    // some query of the wave sees a block maximum more than 2^8 above it
-    // (p then stays below 256, far inside the range of bf16 and fp32), and
-    // the rescale of the running sums is skipped for the other blocks.
+    // The softmax is the same for any reference, so a query's m_run only
+    // moves when its block maximum exceeds it by more than 2^8 (p then stays
+    // below 256, far inside the range of bf16 and fp32).  The decision is
+    // the query's own; the rescale runs when any query of the wave moves,
+    // the others multiplying by exactly 1, so a query's result never
+    // depends on which queries share its wave.
     const float m_blk = tmax * scale_log2;
-    if (__builtin_amdgcn_ballot_w64(m_blk > m_run + 8.f) != 0) {
-      const float m_new = fmaxf(m_run, m_blk);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first block
-      m_run = m_new;
+    const bool grow = m_blk > m_run + 8.f;  // always on the first block
+    if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+      const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_blk) : 1.f;  // 0 on the first block
+      m_run = grow ? m_blk : m_run;
       l_run *= alpha;
 #pragma unroll
       for (int t = 0; t < DT; ++t)
@@ -351,9 +353,15 @@ static hipError_t attn_launch(int dtype, const void* q, const void* k, const voi
                               int n_slots, int H, int seq, int per_slot, hipStream_t st) {
   const float scale_log2 = kLog2e / sqrtf(static_cast<float>(DH));
   if (dtype == DT_BF16) {
-    // 64 queries per workgroup: 128 streams each slot's keys and values
-    // fewer times but measured no faster inside the MAR-L schedule
-    attn_bf16_launch<DH, 2>(q, k, v, out, n_slots, H, seq, per_slot, scale_log2, st);
+    // 128 queries per workgroup share each key/value block four ways and,
+    // with half the prefetch registers per thread, fit three waves per SIMD
+    // for d_head <= 64; below 128 queries per slot the empty query rows of
+    // such a workgroup cost more (measured on MI355X: dense MAR-L -17 %,
+    // 50-query launches +18 %, d_head 80 +8 %)
+    if (per_slot >= 128 && DH <= 64)
+      attn_bf16_launch<DH, 4>(q, k, v, out, n_slots, H, seq, per_slot, scale_log2, st);
+    else
+      attn_bf16_launch<DH, 2>(q, k, v, out, n_slots, H, seq, per_slot, scale_log2, st);
   } else {
     const int qblocks = (per_slot + 63) / 64;
     const long grid = static_cast<long>(n_slots) * H * qblocks;

@@ -263,14 +263,48 @@ def test_attention(dtype, S, dh, H, per):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_attention_query_rows_independent(dtype):
+@pytest.mark.parametrize("per", [320, 50])
+def test_attention_spiky_keys(dtype, per):
+    """Keys past the first blocks that score far above (or below) all
+    earlier ones move the running softmax maxima mid-sequence; against the
+    oracle for the dense and a partial launch."""
+    slots, H, S, dh = 2, 2, 320, 64
+    D = H * dh
+    q = normal_rows((slots * per, D), seed=58, dtype=dtype)
+    k = normal_rows((slots, H, S, dh), seed=59, dtype=dtype)
+    k[:, :, 200:204] *= 12.0
+    k[:, :, 290:292] *= 20.0
+    k = to_storage(k, dtype)
+    v = normal_rows((slots, H, S, dh), seed=60, dtype=dtype)
+    td = to_device(q[:1], dtype).dtype
+    out = torch.empty((slots * per, D), dtype=td, device=DEV)
+    B.k_attention(dtype, to_device(q, dtype), to_device(k, dtype), to_device(v, dtype), out, slots, H, S, dh, per)
+    torch.cuda.synchronize()
+    ref = np.empty((slots * per, D))
+    for s in range(slots):
+        for h in range(H):
+            ref[s * per:(s + 1) * per, h * dh:(h + 1) * dh] = O.attention(
+                q[s * per:(s + 1) * per, h * dh:(h + 1) * dh], k[s, h], v[s, h])
+    _close(out, ref, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("spiky", [False, True])
+def test_attention_query_rows_independent(dtype, spiky):
     """A query's result does not depend on the other queries of the launch:
-    the partial launch reproduces the dense launch's rows bit for bit."""
+    the partial launch (other queries per workgroup and wave) reproduces the
+    dense launch's rows bit for bit.  With spiky keys, a few keys past the
+    first block score far above everything before them for some queries and
+    far below for others, so the running maxima move mid-sequence for only
+    part of each wave."""
     slots, H, S, dh = 2, 2, 200, 64
     D = H * dh
     q = normal_rows((slots * S, D), seed=54, dtype=dtype)
     k = normal_rows((slots, H, S, dh), seed=55, dtype=dtype)
     v = normal_rows((slots, H, S, dh), seed=56, dtype=dtype)
+    if spiky:
+        k[:, :, 130:136] *= 12.0
+        k = to_storage(k, dtype)
     kd, vd = to_device(k, dtype), to_device(v, dtype)
     td = kd.dtype
     dense = torch.empty((slots * S, D), dtype=td, device=DEV)
