@@ -80,18 +80,20 @@ __device__ __forceinline__ float gelu_erf(float x) {
 // Stegun formula 7.1.27:
 //   erf(z) = 1 - 1 / (1 + a1 z + a2 z^2 + a3 z^3 + a4 z^4)^4,  z >= 0,
 //   |error| <= 5e-4,
-// so q = (1 - erf) / 2 = 0.5 / D^4: one reciprocal, no exponential.  The
-// error in gelu is at most 2.5e-4 |x|, a sixteenth of a bf16 rounding step.
+// so with z = |x| / sqrt(2), q = (1 - erf(z)) / 2 = 1 / (2^(1/4) D)^4: the
+// polynomial is taken in |x| with its coefficients scaled by 2^(1/4) and
+// powers of 1/sqrt(2), and one reciprocal gives q.  gelu = x (1 - q) for
+// x >= 0 and x q for x < 0, which is max(x, 0) - |x| q for both signs.
+// The error in gelu is at most 2.4e-4 |x|, a sixteenth of a bf16 step.
 __device__ __forceinline__ float gelu_erf_bf16(float x) {
-  const float z = fabsf(x) * 0.70710678118654752440f;
-  float d = fmaf(0.078108f, z, 0.000972f);
-  d = fmaf(d, z, 0.230389f);
-  d = fmaf(d, z, 0.278393f);
-  d = fmaf(d, z, 1.0f);
+  const float ax = fabsf(x);
+  float d = fmaf(0.0232216473f, ax, 0.000408675658f);  // 2^(1/4) (a4 / 4, a3 / 2^(3/2))
+  d = fmaf(d, ax, 0.136990119f);                       // 2^(1/4) a2 / 2
+  d = fmaf(d, ax, 0.234099676f);                       // 2^(1/4) a1 / 2^(1/2)
+  d = fmaf(d, ax, 1.18920712f);                        // 2^(1/4)
   const float r = __builtin_amdgcn_rcpf(d);
   const float r2 = r * r;
-  const float xq = (0.5f * x) * (r2 * r2);  // x q
-  return x >= 0.0f ? x - xq : xq;
+  return fmaf(-(ax * r2), r2, fmaxf(x, 0.0f));
 }
 
 typedef __attribute__((ext_vector_type(4))) int i32x4_t;
