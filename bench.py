@@ -38,6 +38,9 @@ def parse():
                     help="kernel class timed with HIP events for the roofline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--decode-steps", type=int, default=64)
+    ap.add_argument("--rule", default="least", choices=list(RULES),
+                    help="token selection of the cached steps (Table 3): least / most similar on the "
+                         "device, or random / token-type rows chosen on the host")
     ap.add_argument("--fc1-shapes", action="store_true",
                     help="only run the fc1 product once per shape the 64-step MAR-L schedule "
                          "launches (for hardware-counter runs) and print each shape's launches per "
@@ -150,6 +153,46 @@ def cpu_baseline(dims, W, recipe, n, plans):
     }
 
 
+# token-selection rules of the cached steps (Table 3's strategies)
+RULES = {
+    "least": "least similar computed (strategy V, LazyMAR)",
+    "most": "most similar computed (strategy IV)",
+    "random": "random rows (strategy III)",
+    "decoded": "decoded tokens computed first (strategy I)",
+    "undecoded": "not-yet-decoded tokens computed first (strategy II)",
+}
+
+
+def given_rows(rule, recipe, plans, slots, seq, n):
+    """Host-chosen rows of every cached step for the random and token-type
+    rules, in pinned host memory so that the step's upload stays
+    asynchronous.  Buffer (condition) rows count as decoded."""
+    import numpy as np
+    import torch
+
+    from paper_2503_12450_amd import schedule as sch
+    from paper_2503_12450_amd import selection as SEL
+    from paper_2503_12450_amd.workload import decoded_mask
+
+    rng = np.random.Generator(np.random.Philox(4))
+    out = {}
+    for i, p in enumerate(plans):
+        if p.mode == sch.FULL:
+            continue
+        if rule == "random":
+            rows = SEL.random_rows(slots, seq, n, rng)
+        else:
+            img = decoded_mask(recipe, i)                       # [images, T]
+            known = np.ones((img.shape[0], seq), dtype=bool)
+            known[:, seq - img.shape[1]:] = img
+            mask = np.concatenate([known, known])[:slots]     # both pathways share the state
+            rows = SEL.observation_rows(mask, n, SEL.COMPUTE_DECODED if rule == "decoded"
+                                        else SEL.COMPUTE_UNDECODED)
+        t = torch.from_numpy(rows).pin_memory()
+        out[i] = (t, t.numpy())
+    return out
+
+
 def main():
     args = parse()
     if args.calibrate_copy:
@@ -190,13 +233,18 @@ def main():
     guided = torch.empty((images, dims.seq_len, dims.d_model), dtype=torch.float32, device=dev)
     scale = 4.0
 
-    def one_step(p, x, ev=None):
+    given = given_rows(args.rule, recipe, plans, 2 * images, dims.seq_len, n) \
+        if args.rule in ("random", "decoded", "undecoded") else {}
+    ranked = B.MAR_TOKEN_CACHED_MOST_SIMILAR if args.rule == "most" else B.MAR_TOKEN_CACHED
+
+    def one_step(i, p, x):
+        slots = 2 * images if p.branches == sch.BOTH else images
         if p.mode == sch.FULL:
             cache.step(x, B.MAR_FULL)
-        elif p.branches == sch.BOTH:
-            cache.step(x, B.MAR_TOKEN_CACHED, n)
+        elif i in given:
+            cache.step(x[:slots], B.MAR_TOKEN_GIVEN, n, slot0=0, sel_idx=given[i][1][:slots])
         else:
-            cache.step(x[:images], B.MAR_TOKEN_CACHED, n, slot0=0)
+            cache.step(x[:slots], ranked, n, slot0=0)
         if p.cfg == sch.STORE:
             cache.cfg_combine(B.MAR_CFG_STORE, Y[:images], Y[images:2 * images], scale, guided)
         else:
@@ -206,7 +254,7 @@ def main():
         for i, p in enumerate(plans):
             if step_events is not None:
                 step_events[i][0].record()
-            one_step(p, X[i])
+            one_step(i, p, X[i])
             if step_events is not None:
                 step_events[i][1].record()
 
@@ -262,6 +310,7 @@ def main():
         "config": {"workload": wl.name, "images": images, "seq_len": dims.seq_len,
                    "n_recompute": n, "decode_steps": len(plans),
                    "schedule": "start 5, tau 9, " + cfg_rule + " guidance reuse",
+                   "selection": RULES[args.rule],
                    "step": "one 64-decoding-step schedule"},
         "tflops": sched_flops / (ms_per_sched / 1e3) / 1e12,
         "step_ms": mean,

@@ -77,7 +77,12 @@ typedef enum {
   /* As MAR_TOKEN_CACHED, but the computed rows are given by the caller
    * (host array, see mar_step) instead of the similarity ranking, as in the
    * random / token-type strategies the paper compares against (Table 3). */
-  MAR_TOKEN_GIVEN = 2
+  MAR_TOKEN_GIVEN = 2,
+  /* As MAR_TOKEN_CACHED with the opposite ranking: the n_recompute MOST
+   * similar rows are computed and the least similar ones taken from the
+   * cache (Table 3, the strategy that caches the minimum-similarity
+   * tokens). */
+  MAR_TOKEN_CACHED_MOST_SIMILAR = 3
 } mar_mode;
 
 typedef enum {
@@ -141,8 +146,9 @@ mar_status mar_cache_init(const mar_dims* dims, const mar_block_weights* blocks,
  *               MAR_E_STATE).
  *  n_recompute  N, rows computed per slot in blocks P..L-1 (0 <= N <= S);
  *               ignored by MAR_FULL.
- *  sel_idx      MAR_TOKEN_CACHED: device [n_slots, N] int32 or NULL; receives
- *               the computed rows of each slot in ascending token order.
+ *  sel_idx      MAR_TOKEN_CACHED / MAR_TOKEN_CACHED_MOST_SIMILAR: device
+ *               [n_slots, N] int32 or NULL; receives the computed rows of
+ *               each slot in ascending token order.
  *               MAR_TOKEN_GIVEN: HOST [n_slots, N] int32, required; each
  *               slot's rows strictly ascending in [0, S) (else MAR_E_ARG);
  *               it must stay unchanged until the stream has passed this
@@ -150,7 +156,9 @@ mar_status mar_cache_init(const mar_dims* dims, const mar_block_weights* blocks,
  *
  * Selection (MAR_TOKEN_CACHED): per slot, the N rows whose value rows of
  * block P-1 (of block 0, formed from x, when P = 0) have the smallest fp64
- * cosine similarity to the slot's previous step; ties to the lower index.
+ * cosine similarity to the slot's previous step; ties to the lower index,
+ * NaN last.  MAR_TOKEN_CACHED_MOST_SIMILAR: the N largest similarities,
+ * ties to the lower index, NaN last.
  * Every mode replaces the slot's scoring reference with this step's value
  * rows. */
 mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0,

@@ -93,6 +93,13 @@ mar_status mar_k_scores(int32_t dtype, const void* v_cur, void* v_ref, int32_t n
 mar_status mar_k_select(const double* scores, int32_t n_slots, int32_t seq, int32_t n, int32_t* idx,
                         void* stream);
 
+/* The opposite ranking (Table 3, the strategy that caches the
+ * minimum-similarity tokens): idx[slot, 0..n) = the n tokens of the slot
+ * with the largest score (NaN ranks last, ties to the lower index),
+ * ascending.  seq <= 4096. */
+mar_status mar_k_select_most_similar(const double* scores, int32_t n_slots, int32_t seq, int32_t n,
+                                     int32_t* idx, void* stream);
+
 /* Tuning hook: force tile configuration `variant` (0 .. MAR_GEMM_VARIANTS-1)
  * for every later matrix product of the process, or -1 to restore the
  * choice by shape.  Every configuration uses the same MFMA instruction and

@@ -17,6 +17,7 @@ from .mar_oracle import (  # noqa: F401
     layer_norm,
     linear,
     select_least_similar,
+    select_most_similar,
     storage_round,
     value_rows,
 )

@@ -26,6 +26,9 @@ Readings of the paper taken here (the paper is silent or garbled on them):
   rounded fp64 sum, so the score does not depend on a summation order.  Zero norms: 1 when both rows are zero, else
   0.  A NaN score ranks as +inf (most similar).
 * Ties go to the lower token index; selected indices are returned ascending.
+* Table 3's strategy that caches the minimum-similarity tokens is taken as
+  its exact opposite: the n *most* similar tokens are computed, ties to the
+  lower index, a NaN score ranked last (never preferred).
 * Rows that are not computed keep the cached state of the previous block's
   output from the first cached block on, so their keys/values come from the
   cache (Eq. 9 applied from block P on).
@@ -187,6 +190,22 @@ def select_least_similar(s, n: int) -> np.ndarray:
     return np.sort(order[:n]).astype(np.int32)
 
 
+def select_most_similar(s, n: int) -> np.ndarray:
+    """Table 3's strategy that caches the minimum-similarity tokens: the n
+    tokens with the largest similarity are computed instead.
+
+    Ties go to the lower token index; NaN ranks last.  Ascending order
+    (int32).
+    """
+    s = np.array(s, dtype=np.float64)
+    if not 0 <= n <= s.shape[-1]:
+        raise ValueError("n out of range")
+    key = -s
+    key[np.isnan(key)] = np.inf
+    order = np.argsort(key, kind="stable")
+    return np.sort(order[:n]).astype(np.int32)
+
+
 def cfg_store(y_cond, y_uncond, scale: float):
     """Refresh step of the condition cache (Eq. 10): returns (stored
     residual C = u - c, guided output u + s (c - u))."""
@@ -255,14 +274,15 @@ class MarOracle:
         self.hc[b] = hc
         return h
 
-    def cached_slot(self, b: int, x, n: int, given: Optional[np.ndarray] = None):
+    def cached_slot(self, b: int, x, n: int, given: Optional[np.ndarray] = None, rule: str = "least"):
         """Cached step of one sequence (Sec. 3.2, Eq. 8 and 9).
 
         Blocks 0..P-1 run on every row; the value rows of block P-1 are scored
-        against the previous step's; the n least similar rows (or the
-        ``given`` rows) are computed through blocks P..L-1 and every other row
-        is taken from the cache.  Returns (output rows of every token, the
-        computed set, the scores).
+        against the previous step's; the n least similar rows (the n most
+        similar with rule="most", Table 3; or the ``given`` rows) are
+        computed through blocks P..L-1 and every other row is taken from the
+        cache.  Returns (output rows of every token, the computed set, the
+        scores).
         """
         if self.hc[b] is None:
             raise RuntimeError("cached step before a full step filled the cache")
@@ -276,7 +296,9 @@ class MarOracle:
         v = storage_round(v, self.dtype)
         scores = cosine_scores(v, self.vref[b])
         if given is None:
-            idx = select_least_similar(scores, n)
+            if rule not in ("least", "most"):
+                raise ValueError("rule is 'least' or 'most'")
+            idx = select_least_similar(scores, n) if rule == "least" else select_most_similar(scores, n)
         else:
             idx = np.asarray(given, dtype=np.int32)
         self.vref[b] = v
@@ -293,12 +315,12 @@ class MarOracle:
         x = _f64(x)
         return np.stack([self.full_slot(slot0 + i, x[i]) for i in range(x.shape[0])])
 
-    def cached(self, x, n: int, slot0: int = 0, given=None):
+    def cached(self, x, n: int, slot0: int = 0, given=None, rule: str = "least"):
         x = _f64(x)
         ys, idxs, ss = [], [], []
         for i in range(x.shape[0]):
             g = None if given is None else np.asarray(given)[i]
-            y, idx, s = self.cached_slot(slot0 + i, x[i], n, g)
+            y, idx, s = self.cached_slot(slot0 + i, x[i], n, g, rule)
             ys.append(y)
             idxs.append(idx)
             ss.append(s)

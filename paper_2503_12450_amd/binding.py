@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libmarcache.so")
 
 MAR_OK, MAR_E_ARG, MAR_E_SHAPE, MAR_E_STATE, MAR_E_WORKSPACE, MAR_E_DEVICE = 0, -1, -2, -3, -4, -5
 MAR_F32, MAR_BF16 = 0, 1
-MAR_FULL, MAR_TOKEN_CACHED, MAR_TOKEN_GIVEN = 0, 1, 2
+MAR_FULL, MAR_TOKEN_CACHED, MAR_TOKEN_GIVEN, MAR_TOKEN_CACHED_MOST_SIMILAR = 0, 1, 2, 3
 MAR_CFG_STORE, MAR_CFG_REUSE = 0, 1
 PROF_KINDS = ("qkv", "proj", "fc1", "fc2", "attention", "layernorm", "scores", "select", "cfg")
 
@@ -29,7 +29,8 @@ EXPORTED = (
     "mar_workspace_bytes", "mar_cache_init", "mar_step", "mar_cfg_combine", "mar_output",
     "mar_cache_destroy", "mar_last_error", "mar_profile_start", "mar_profile_stop",
     "mar_k_layernorm", "mar_k_linear", "mar_k_linear_residual", "mar_k_qkv",
-    "mar_k_attention", "mar_k_scores", "mar_k_select", "mar_k_gemm_variant",
+    "mar_k_attention", "mar_k_scores", "mar_k_select", "mar_k_select_most_similar",
+    "mar_k_gemm_variant",
 )
 GEMM_VARIANTS = 12
 
@@ -78,6 +79,7 @@ _SIGNATURES = {
     "mar_k_attention": (_i32, [_i32, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp]),
     "mar_k_scores": (_i32, [_i32, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _i32, _vp]),
     "mar_k_select": (_i32, [_vp, _i32, _i32, _i32, _vp, _vp]),
+    "mar_k_select_most_similar": (_i32, [_vp, _i32, _i32, _i32, _vp, _vp]),
     "mar_k_gemm_variant": (_i32, [_i32]),
 }
 
@@ -274,9 +276,10 @@ def k_scores(dtype: str, v_cur, v_ref, scores, update_ref: bool = False, stream=
                                seq, d_head, scores.data_ptr(), 1 if update_ref else 0, _stream(stream)))
 
 
-def k_select(scores, n: int, idx, stream=None) -> None:
+def k_select(scores, n: int, idx, stream=None, most_similar: bool = False) -> None:
     n_slots, seq = scores.shape
-    _check(load().mar_k_select(scores.data_ptr(), n_slots, seq, n, idx.data_ptr(), _stream(stream)))
+    fn = load().mar_k_select_most_similar if most_similar else load().mar_k_select
+    _check(fn(scores.data_ptr(), n_slots, seq, n, idx.data_ptr(), _stream(stream)))
 
 
 def k_gemm_variant(variant: int) -> None:

@@ -460,7 +460,8 @@ mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0, in
   if (!aligned16(x)) return fail(MAR_E_ARG, "x must be 16-byte aligned");
   if (slot0 < 0 || n_slots < 1 || slot0 > d.max_slots - n_slots)
     return fail(MAR_E_ARG, "slots [%d, %d) outside [0, %d)", slot0, slot0 + n_slots, d.max_slots);
-  if (mode != MAR_FULL && mode != MAR_TOKEN_CACHED && mode != MAR_TOKEN_GIVEN)
+  if (mode != MAR_FULL && mode != MAR_TOKEN_CACHED && mode != MAR_TOKEN_GIVEN &&
+      mode != MAR_TOKEN_CACHED_MOST_SIMILAR)
     return fail(MAR_E_ARG, "unknown mode %d", mode);
   const int S = d.seq_len;
   const int N = n_recompute;
@@ -558,9 +559,9 @@ mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0, in
     int32_t* idx = cache->at<int32_t>(lay.idx);
     TIMED(MAR_PROF_SCORES, 0, 3.0 * Mfull * c.D * c.es + 8.0 * Mfull,
           launch_scores(c.dtype, vcur, vref, n_slots, c.H, S, c.dh, scores, true, c.st), "scores");
-    if (mode == MAR_TOKEN_CACHED) {
+    if (mode == MAR_TOKEN_CACHED || mode == MAR_TOKEN_CACHED_MOST_SIMILAR) {
       TIMED(MAR_PROF_SELECT, 0, 8.0 * Mfull + 4.0 * n_slots * N,
-            launch_select(scores, n_slots, S, N, idx, c.st), "select");
+            launch_select(scores, n_slots, S, N, mode == MAR_TOKEN_CACHED_MOST_SIMILAR, idx, c.st), "select");
       if (sel_idx && N > 0)
         STEP_HIP(hipMemcpyAsync(sel_idx, idx, sizeof(int32_t) * n_slots * N, hipMemcpyDeviceToDevice,
                                 c.st),
@@ -795,13 +796,23 @@ mar_status mar_k_scores(int32_t dtype, const void* v_cur, void* v_ref, int32_t n
   return MAR_OK;
 }
 
-mar_status mar_k_select(const double* scores, int32_t n_slots, int32_t seq, int32_t n, int32_t* idx,
-                        void* stream) {
+static mar_status select_rule(const double* scores, int32_t n_slots, int32_t seq, int32_t n, bool largest,
+                              int32_t* idx, void* stream) {
   g_err.clear();
   if (!scores || (!idx && n > 0 && n_slots > 0)) return fail(MAR_E_ARG, "NULL pointer");
   if (n_slots < 0 || seq < 1 || seq > kMaxSeq || n < 0 || n > seq) return fail(MAR_E_SHAPE, "bad sizes");
-  MAR_HIP(launch_select(scores, n_slots, seq, n, idx, static_cast<hipStream_t>(stream)), "select");
+  MAR_HIP(launch_select(scores, n_slots, seq, n, largest, idx, static_cast<hipStream_t>(stream)), "select");
   return MAR_OK;
+}
+
+mar_status mar_k_select(const double* scores, int32_t n_slots, int32_t seq, int32_t n, int32_t* idx,
+                        void* stream) {
+  return select_rule(scores, n_slots, seq, n, false, idx, stream);
+}
+
+mar_status mar_k_select_most_similar(const double* scores, int32_t n_slots, int32_t seq, int32_t n,
+                                     int32_t* idx, void* stream) {
+  return select_rule(scores, n_slots, seq, n, true, idx, stream);
 }
 
 mar_status mar_k_gemm_variant(int32_t variant) {

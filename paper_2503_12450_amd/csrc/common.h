@@ -162,8 +162,9 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
 hipError_t launch_scores(int dtype, const void* v_cur, void* v_ref, int n_slots, int H,
                          int seq, int dh, double* scores, bool update_ref, hipStream_t st);
 
-// The n least similar tokens of each slot, ascending.
-hipError_t launch_select(const double* scores, int n_slots, int seq, int n, int32_t* idx,
+// The n least similar tokens of each slot (the n most similar when
+// `largest`), ascending.
+hipError_t launch_select(const double* scores, int n_slots, int seq, int n, bool largest, int32_t* idx,
                          hipStream_t st);
 
 // Guidance with the condition cache over `count` fp32 elements.

@@ -16,6 +16,8 @@
 //   ties to the lower index), written in ascending token order.  A token's
 //   rank is the number of tokens before it in the strict total order
 //   (score, index); ranks are a permutation, so exactly n tokens are chosen.
+//   The opposite rule (the n largest scores: Table 3's strategy that caches
+//   the least similar tokens) ranks by (-score, index), NaN again last.
 #include "common.h"
 
 namespace marcache {
@@ -96,15 +98,15 @@ __global__ __launch_bounds__(256) void scores_kernel(const T* __restrict__ v_cur
 
 // One workgroup of 256 threads per slot; scores staged in LDS.
 __global__ __launch_bounds__(256) void select_kernel(const double* __restrict__ scores, int seq,
-                                                     int n, int32_t* __restrict__ idx) {
+                                                     int n, int largest, int32_t* __restrict__ idx) {
   extern __shared__ double s_lds[];  // [seq] scores, then [256] int counts
   int* cnt = reinterpret_cast<int*>(s_lds + seq);
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   const double* s = scores + static_cast<long>(b) * seq;
   for (int t = tid; t < seq; t += 256) {
-    double v = s[t];
-    if (v != v) v = __builtin_huge_val();  // NaN ranks as +inf
+    double v = largest ? -s[t] : s[t];
+    if (v != v) v = __builtin_huge_val();  // NaN ranks last
     s_lds[t] = v;
   }
   __syncthreads();
@@ -158,11 +160,11 @@ hipError_t launch_scores(int dtype, const void* v_cur, void* v_ref, int n_slots,
   return hipGetLastError();
 }
 
-hipError_t launch_select(const double* scores, int n_slots, int seq, int n, int32_t* idx,
+hipError_t launch_select(const double* scores, int n_slots, int seq, int n, bool largest, int32_t* idx,
                          hipStream_t st) {
   if (n_slots == 0 || n == 0) return hipSuccess;
   const size_t lds = static_cast<size_t>(seq) * sizeof(double) + 256 * sizeof(int);
-  hipLaunchKernelGGL(select_kernel, dim3(n_slots), dim3(256), lds, st, scores, seq, n, idx);
+  hipLaunchKernelGGL(select_kernel, dim3(n_slots), dim3(256), lds, st, scores, seq, n, largest ? 1 : 0, idx);
   return hipGetLastError();
 }
 

@@ -348,7 +348,10 @@ def test_scores_bitwise(dtype, slots, H, S, dh):
 
 @pytest.mark.parametrize("slots,S,n", [(4, 320, 50), (2, 320, 0), (2, 320, 320), (1, 1, 1), (3, 1088, 218),
                                        (2, 4096, 1000), (5, 33, 31)])
-def test_select_bit_exact(slots, S, n):
+@pytest.mark.parametrize("most", [False, True])
+def test_select_bit_exact(slots, S, n, most):
+    """Both ranking rules (least similar: strategy V; most similar: strategy
+    IV of Table 3) bit for bit, with exact ties, NaN and signed zeros."""
     g = np.random.Generator(np.random.Philox(71))
     s = 1.0 - np.abs(g.standard_normal((slots, S))) * 1e-3
     s[0, : S // 3] = np.round(s[0, : S // 3], 4)   # many exact ties
@@ -357,7 +360,8 @@ def test_select_bit_exact(slots, S, n):
         s[-1, 6] = -0.0
         s[-1, 7] = 0.0
     idx = torch.full((slots, n), -1, dtype=torch.int32, device=DEV)
-    B.k_select(torch.from_numpy(s).to(DEV), n, idx)
+    B.k_select(torch.from_numpy(s).to(DEV), n, idx, most_similar=most)
     torch.cuda.synchronize()
-    want = np.stack([O.select_least_similar(s[b], n) for b in range(slots)])
+    rule = O.select_most_similar if most else O.select_least_similar
+    want = np.stack([rule(s[b], n) for b in range(slots)])
     np.testing.assert_array_equal(idx.cpu().numpy(), want)

@@ -52,13 +52,14 @@ def _step(cache, x, mode, n=0, slot0=0, given=None):
     xd = to_device(x, cache.dims.dtype)
     y = torch.empty((x.shape[0], cache.dims.seq_len, cache.dims.d_model), dtype=torch.float32, device=DEV)
     sel = None
-    if mode == B.MAR_TOKEN_CACHED:
+    ranked = mode in (B.MAR_TOKEN_CACHED, B.MAR_TOKEN_CACHED_MOST_SIMILAR)
+    if ranked:
         sel = torch.full((x.shape[0], max(n, 1)), -1, dtype=torch.int32, device=DEV)
     elif mode == B.MAR_TOKEN_GIVEN:
         sel = given
     cache.step(xd, mode, n, slot0=slot0, y=y, sel_idx=sel)
     torch.cuda.synchronize()
-    idx = sel[:, :n].cpu().numpy() if mode == B.MAR_TOKEN_CACHED else None
+    idx = sel[:, :n].cpu().numpy() if ranked else None
     return y, idx
 
 
@@ -114,6 +115,54 @@ def test_config1_noise_selection_matches_oracle():
             assert np.all(so[b][idx[b]] <= thr + 1e-9)
     if np.array_equal(idx, idxo):
         np.testing.assert_allclose(_host(y), yo, **TOL["f32"])
+
+
+@pytest.mark.parametrize("name", ["f32-block-P0", "bf16-P0"])
+def test_most_similar_rule_matches_oracle(name):
+    """Table 3's opposite ranking (the n most similar rows computed).  With
+    no always-computed block the value rows depend on each token's own input
+    only, so the construction is exact: n rows per slot change by small
+    noise and all others by large noise, and the n most similar rows are the
+    small-noise ones on both sides."""
+    dims = SMALL[name]
+    n = max(1, dims.seq_len // 5)
+    W, cache = _make(dims)
+    slots = dims.max_slots
+    x = normal_rows((slots, dims.seq_len, dims.d_model), seed=5, dtype=dims.dtype)
+    near = random_index_sets(slots, dims.seq_len, n, seed=6)
+    small = normal_rows(x.shape, seed=7, std=0.2)
+    large = normal_rows(x.shape, seed=8, std=3.0)
+    prev = x + large
+    for b in range(slots):
+        prev[b, near[b]] = x[b, near[b]] + small[b, near[b]]
+    prev = to_storage(prev, dims.dtype)
+    orc = O.MarOracle(dims, W)
+    _step(cache, prev, B.MAR_FULL)
+    orc.full(prev)
+    y, idx = _step(cache, x, B.MAR_TOKEN_CACHED_MOST_SIMILAR, n)
+    yo, idxo, so = orc.cached(x, n, rule="most")
+    np.testing.assert_array_equal(idxo, np.sort(near, axis=1))  # the construction is well conditioned
+    np.testing.assert_array_equal(idx, idxo)
+    np.testing.assert_allclose(_host(y), yo, **TOL[dims.dtype])
+
+
+@pytest.mark.parametrize("compute", ["decoded", "undecoded"])
+def test_token_type_rule_through_given_rows(compute):
+    """Table 3's token-type strategies: the host rule picks the rows from the
+    sampler's decoded mask, the step computes them as given rows."""
+    from paper_2503_12450_amd import selection as SEL
+    dims = SMALL["bf16-stack-P2"]
+    n = dims.seq_len // 4
+    W, cache = _make(dims)
+    x, prev, _ = _gap_inputs(dims, dims.max_slots, n)
+    decoded = np.random.default_rng(9).random((dims.max_slots, dims.seq_len)) < 0.3
+    rows = SEL.observation_rows(decoded, n, compute)
+    orc = O.MarOracle(dims, W)
+    _step(cache, prev, B.MAR_FULL)
+    orc.full(prev)
+    y, _ = _step(cache, x, B.MAR_TOKEN_GIVEN, n, given=rows)
+    yo, _, _ = orc.cached(x, n, given=rows)
+    np.testing.assert_allclose(_host(y), yo, **TOL[dims.dtype])
 
 
 @pytest.mark.parametrize("name", ["bf16-stack-P2", "f32-stack-P1", "bf16-P0"])

@@ -14,7 +14,7 @@ import torch
 from scipy.spatial.distance import cosine as scipy_cosine
 
 from oracle import (MarOracle, attention, block_rows, cfg_reuse, cfg_store,
-                    cosine_scores, gelu, guided, layer_norm, select_least_similar,
+                    cosine_scores, gelu, guided, layer_norm, select_least_similar, select_most_similar,
                     storage_round, value_rows)
 from paper_2503_12450_amd.workload import MarDims, all_block_weights, normal_rows, perturbed
 
@@ -234,6 +234,44 @@ def test_select_special_cases():
     assert a == b
     with pytest.raises(ValueError):
         select_least_similar(s, 6)
+
+
+def _brute_select_most(s, n):
+    """The n-subset with the largest score sum; among equal sums the
+    lexicographically smallest index tuple (ties to the lower index)."""
+    best = None
+    for c in itertools.combinations(range(len(s)), n):
+        key = (-sum(s[i] for i in c), c)
+        if best is None or key < best:
+            best = key
+    return np.array(best[1] if best else (), dtype=np.int32)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_select_most_similar_brute_force_with_ties(seed):
+    rng = np.random.default_rng(100 + seed)
+    S = int(rng.integers(1, 10))
+    s = rng.integers(-8, 9, size=S) / 8.0
+    for n in range(S + 1):
+        np.testing.assert_array_equal(select_most_similar(s, n), _brute_select_most(list(s), n))
+
+
+def test_select_most_similar_special_cases():
+    s = np.array([0.3, 0.1, 0.9, 0.1, 0.5])
+    assert select_most_similar(s, 0).size == 0
+    np.testing.assert_array_equal(select_most_similar(s, 2), [2, 4])
+    np.testing.assert_array_equal(select_most_similar(s, 4), [0, 1, 2, 4])  # the tie goes to index 1
+    np.testing.assert_array_equal(select_most_similar(np.ones(7), 3), [0, 1, 2])
+    # NaN ranks last under this rule too
+    np.testing.assert_array_equal(select_most_similar(np.array([np.nan, 0.5, 0.7]), 2), [1, 2])
+    np.testing.assert_array_equal(select_most_similar(np.array([np.nan, 0.5, 0.7]), 3), [0, 1, 2])
+    # distinct scores: the complement of the least-similar rule
+    t = np.random.default_rng(3).standard_normal(50)
+    for n in (0, 1, 17, 49, 50):
+        comp = np.setdiff1d(np.arange(50), select_least_similar(t, 50 - n))
+        np.testing.assert_array_equal(select_most_similar(t, n), comp)
+    with pytest.raises(ValueError):
+        select_most_similar(s, 6)
 
 
 # --------------------------------------------------------------------------
