@@ -38,6 +38,10 @@ def parse():
                     help="kernel class timed with HIP events for the roofline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--decode-steps", type=int, default=64)
+    ap.add_argument("--score-source", default="values", choices=["values", "features"],
+                    help="what the similarity compares (Sec. 4.4): block P-1's value rows or its output features")
+    ap.add_argument("--fresh-kv", action="store_true",
+                    help="recompute every row's keys/values at the first cached block")
     ap.add_argument("--rule", default="least", choices=list(RULES),
                     help="token selection of the cached steps (Table 3): least / most similar on the "
                          "device, or random / token-type rows chosen on the host")
@@ -216,8 +220,10 @@ def main():
     from paper_2503_12450_amd.device import upload_blocks
     from paper_2503_12450_amd.workload import WORKLOADS, all_block_weights, decode_recipe, step_inputs_device
 
+    from dataclasses import replace
     wl = WORKLOADS[args.workload]
-    dims, n, images = wl.dims, wl.n_recompute, wl.images
+    dims = replace(wl.dims, score_source=args.score_source, fresh_kv=args.fresh_kv)
+    n, images = wl.n_recompute, wl.images
     dev = "cuda:0"
     torch.cuda.set_device(0)
     W = all_block_weights(dims)
@@ -311,6 +317,7 @@ def main():
                    "n_recompute": n, "decode_steps": len(plans),
                    "schedule": "start 5, tau 9, " + cfg_rule + " guidance reuse",
                    "selection": RULES[args.rule],
+                   "score_source": args.score_source, "fresh_kv": args.fresh_kv,
                    "step": "one 64-decoding-step schedule"},
         "tflops": sched_flops / (ms_per_sched / 1e3) / 1e12,
         "step_ms": mean,

@@ -96,16 +96,33 @@ typedef enum {
  * Supported: d_model % n_heads == 0, d_head = d_model / n_heads a multiple
  * of 16 and at most 128, d_model and d_mlp multiples of 64, 1 <= seq_len <=
  * 4096, d_model <= 2048, max_slots >= 1, 0 <= full_prefix < n_layers. */
+/* What the similarity of Eq. (8) compares, step to step (Sec. 4.4). */
+typedef enum {
+  MAR_SCORE_VALUES = 0,  /* the self-attention value rows of block P-1 (of
+                            block 0, formed from x, when P = 0): the paper's
+                            choice */
+  MAR_SCORE_FEATURES = 1 /* the features: block P-1's output rows (fp32), or
+                            the step input x when P = 0 */
+} mar_score_source;
+
+/* Zero-initialize, then set the fields: the trailing options default to the
+ * paper's method. */
 typedef struct {
-  int32_t n_layers;    /* L */
-  int32_t d_model;     /* D */
-  int32_t n_heads;     /* H */
-  int32_t d_mlp;       /* F */
-  int32_t seq_len;     /* S: buffer/class rows + image-token rows */
-  int32_t max_slots;   /* sequence slots held by the caches */
-  int32_t full_prefix; /* P: blocks always computed on every row (paper: 3) */
-  int32_t dtype;       /* mar_dtype */
-  float ln_eps;        /* LayerNorm epsilon */
+  int32_t n_layers;     /* L */
+  int32_t d_model;      /* D */
+  int32_t n_heads;      /* H */
+  int32_t d_mlp;        /* F */
+  int32_t seq_len;      /* S: buffer/class rows + image-token rows */
+  int32_t max_slots;    /* sequence slots held by the caches */
+  int32_t full_prefix;  /* P: blocks always computed on every row (paper: 3) */
+  int32_t dtype;        /* mar_dtype */
+  float ln_eps;         /* LayerNorm epsilon */
+  int32_t score_source; /* mar_score_source */
+  int32_t fresh_kv;     /* 0: at block P the keys/values of the rows that
+                           are not computed come from the cache (Eq. 9);
+                           1: they are recomputed for every row from this
+                           step's block P-1 output (one key/value product
+                           over all rows per cached step) */
 } mar_dims;
 
 /* Device pointers to the parameters of one block, nn.Linear layout
@@ -155,12 +172,13 @@ mar_status mar_cache_init(const mar_dims* dims, const mar_block_weights* blocks,
  *               call.  Ignored by MAR_FULL.
  *
  * Selection (MAR_TOKEN_CACHED): per slot, the N rows whose value rows of
- * block P-1 (of block 0, formed from x, when P = 0) have the smallest fp64
- * cosine similarity to the slot's previous step; ties to the lower index,
- * NaN last.  MAR_TOKEN_CACHED_MOST_SIMILAR: the N largest similarities,
- * ties to the lower index, NaN last.
+ * block P-1 (of block 0, formed from x, when P = 0; the features instead
+ * with MAR_SCORE_FEATURES) have the smallest fp64 cosine similarity to the
+ * slot's previous step; ties to the lower index, NaN last.
+ * MAR_TOKEN_CACHED_MOST_SIMILAR: the N largest similarities, ties to the
+ * lower index, NaN last.
  * Every mode replaces the slot's scoring reference with this step's value
- * rows. */
+ * rows (features). */
 mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0,
                     int32_t n_slots, int32_t mode, int32_t n_recompute,
                     int32_t* sel_idx, void* stream);

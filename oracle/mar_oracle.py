@@ -29,6 +29,15 @@ Readings of the paper taken here (the paper is silent or garbled on them):
 * Table 3's strategy that caches the minimum-similarity tokens is taken as
   its exact opposite: the n *most* similar tokens are computed, ties to the
   lower index, a NaN score ranked last (never preferred).
+* Option score_source = "features" (the alternative Sec. 4.4 weighs against
+  the value matrix; Eq. (8) writes the features of the third layer): the
+  similarity compares the output rows of block P-1 as the path stores its
+  residual stream (float32), or the step input x when no block is always
+  computed.
+* Option fresh_kv (the reading the paper leaves open, taken the other way):
+  at block P the rows that are not computed contribute keys/values formed
+  from this step's block P-1 output instead of the cached ones; their
+  outputs still come from the cache.
 * Rows that are not computed keep the cached state of the previous block's
   output from the first cached block on, so their keys/values come from the
   cache (Eq. 9 applied from block P on).
@@ -249,8 +258,13 @@ class MarOracle:
         if len(blocks) != self.L:
             raise ValueError("one weight dict per block expected")
         self.blocks = list(blocks)
+        self.score_source = getattr(dims, "score_source", "values")
+        self.fresh_kv = bool(getattr(dims, "fresh_kv", False))
+        if self.score_source not in ("values", "features"):
+            raise ValueError("score_source is 'values' or 'features'")
         self.hc: List[Optional[Dict[int, np.ndarray]]] = [None] * self.max_slots
         self.vref: List[Optional[np.ndarray]] = [None] * self.max_slots
+        self.fref: List[Optional[np.ndarray]] = [None] * self.max_slots
         self.delta: Dict[int, np.ndarray] = {}
 
     # -- one sequence ------------------------------------------------------
@@ -265,10 +279,13 @@ class MarOracle:
         hc: Dict[int, np.ndarray] = {}
         if self.P == 0:
             hc[-1] = h.copy()
+            self.fref[b] = h.copy()
         for l in range(self.L):
             h, v = block_rows(h, rows, self.blocks[l], self.H, self.eps)
             if l == self._score_layer():
                 self.vref[b] = storage_round(v, self.dtype)
+            if l == self.P - 1:
+                self.fref[b] = storage_round(h, "f32")
             if l >= self.P - 1:
                 hc[l] = h.copy()
         self.hc[b] = hc
@@ -294,7 +311,12 @@ class MarOracle:
             for l in range(self.P):
                 h, v = block_rows(h, rows_all, self.blocks[l], self.H, self.eps)
         v = storage_round(v, self.dtype)
-        scores = cosine_scores(v, self.vref[b])
+        if self.score_source == "features":
+            feat = h.copy() if self.P == 0 else storage_round(h, "f32")
+            scores = cosine_scores(feat, self.fref[b])
+            self.fref[b] = feat
+        else:
+            scores = cosine_scores(v, self.vref[b])
         if given is None:
             if rule not in ("least", "most"):
                 raise ValueError("rule is 'least' or 'most'")
@@ -303,6 +325,8 @@ class MarOracle:
             idx = np.asarray(given, dtype=np.int32)
         self.vref[b] = v
         hc = self.hc[b]
+        if self.fresh_kv:
+            hc[self.P - 1] = h.copy()  # every row's block-P input (keys/values) from this step
         fresh = h[idx]
         for l in range(self.P, self.L):
             hc[l - 1][idx] = fresh

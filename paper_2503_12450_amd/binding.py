@@ -19,6 +19,7 @@ MAR_OK, MAR_E_ARG, MAR_E_SHAPE, MAR_E_STATE, MAR_E_WORKSPACE, MAR_E_DEVICE = 0, 
 MAR_F32, MAR_BF16 = 0, 1
 MAR_FULL, MAR_TOKEN_CACHED, MAR_TOKEN_GIVEN, MAR_TOKEN_CACHED_MOST_SIMILAR = 0, 1, 2, 3
 MAR_CFG_STORE, MAR_CFG_REUSE = 0, 1
+MAR_SCORE_VALUES, MAR_SCORE_FEATURES = 0, 1
 PROF_KINDS = ("qkv", "proj", "fc1", "fc2", "attention", "layernorm", "scores", "select", "cfg")
 
 STATUS_NAMES = {0: "MAR_OK", -1: "MAR_E_ARG", -2: "MAR_E_SHAPE", -3: "MAR_E_STATE",
@@ -46,7 +47,8 @@ class MarDimsC(ctypes.Structure):
                 ("n_heads", ctypes.c_int32), ("d_mlp", ctypes.c_int32),
                 ("seq_len", ctypes.c_int32), ("max_slots", ctypes.c_int32),
                 ("full_prefix", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("ln_eps", ctypes.c_float)]
+                ("ln_eps", ctypes.c_float), ("score_source", ctypes.c_int32),
+                ("fresh_kv", ctypes.c_int32)]
 
 
 WEIGHT_FIELDS = ("ln1_w", "ln1_b", "qkv_w", "qkv_b", "proj_w", "proj_b",
@@ -111,9 +113,14 @@ def dtype_code(dtype: str) -> int:
     return {"f32": MAR_F32, "bf16": MAR_BF16}[dtype]
 
 
+SCORE_SOURCES = {"values": MAR_SCORE_VALUES, "features": MAR_SCORE_FEATURES}
+
+
 def dims_c(dims) -> MarDimsC:
     return MarDimsC(dims.n_layers, dims.d_model, dims.n_heads, dims.d_mlp, dims.seq_len,
-                    dims.max_slots, dims.full_prefix, dtype_code(dims.dtype), dims.ln_eps)
+                    dims.max_slots, dims.full_prefix, dtype_code(dims.dtype), dims.ln_eps,
+                    SCORE_SOURCES[getattr(dims, "score_source", "values")],
+                    1 if getattr(dims, "fresh_kv", False) else 0)
 
 
 # --------------------------------------------------------------------------

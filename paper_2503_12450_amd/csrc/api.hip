@@ -62,6 +62,9 @@ mar_status check_dims(const mar_dims* d) {
   if (d->full_prefix < 0 || d->full_prefix >= d->n_layers)
     return fail(MAR_E_SHAPE, "full_prefix must be in [0, n_layers)");
   if (!(d->ln_eps > 0.f)) return fail(MAR_E_ARG, "ln_eps must be positive");
+  if (d->score_source != MAR_SCORE_VALUES && d->score_source != MAR_SCORE_FEATURES)
+    return fail(MAR_E_ARG, "unknown score_source %d", d->score_source);
+  if (d->fresh_kv != 0 && d->fresh_kv != 1) return fail(MAR_E_ARG, "fresh_kv must be 0 or 1");
   return MAR_OK;
 }
 
@@ -77,7 +80,7 @@ struct Layout {
   size_t w_qkv = 0, w_proj = 0, w_fc1 = 0, w_fc2 = 0, b_ln1w = 0, b_ln1b = 0, b_ln2w = 0, b_ln2b = 0,
          b_qkv = 0, b_proj = 0, b_fc1 = 0, b_fc2 = 0, layer_bytes = 0;
   std::vector<size_t> kc_off, vc_off;
-  size_t vref = 0, Y = 0, cres = 0;
+  size_t vref = 0, fref = 0, Y = 0, cres = 0;
   size_t h = 0, c = 0, a = 0, q = 0, o = 0, f = 0, ktmp = 0, vtmp = 0, vcur = 0, scores = 0, idx = 0;
 };
 
@@ -115,6 +118,8 @@ Layout make_layout(const mar_dims& d) {
     L.vc_off[l] = take(rows * D * es);
   }
   L.vref = take(rows * D * es);
+  // feature reference: block P-1's fp32 output rows, or x when P = 0
+  if (d.score_source == MAR_SCORE_FEATURES) L.fref = take(rows * D * (d.full_prefix == 0 ? es : 4));
   L.Y = take(rows * D * 4);
   const size_t pairs = (NS + 1) / 2;
   L.cres = take(pairs * S * D * 4);
@@ -508,9 +513,20 @@ mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0, in
   void* vtmp = cache->at<void>(lay.vtmp);
   void* vcur = cache->at<void>(lay.vcur);
   const int score_layer = c.P > 0 ? c.P - 1 : 0;
+  // feature scoring (Sec. 4.4 alternative): block P-1's fp32 output rows,
+  // or x (storage dtype) when P = 0, against the previous step's
+  const bool features = d.score_source == MAR_SCORE_FEATURES;
+  const size_t fes = c.P == 0 ? c.es : 4;
+  void* fref = features ? static_cast<char*>(cache->at<void>(lay.fref)) +
+                              static_cast<size_t>(slot0) * S * c.D * fes
+                        : nullptr;
+  float* hbuf = cache->at<float>(lay.h);
+  const size_t feat_bytes = static_cast<size_t>(n_slots) * S * c.D * fes;
   mar_status s;
 
   if (mode == MAR_FULL) {
+    if (features && c.P == 0)
+      STEP_HIP(hipMemcpyAsync(fref, x, feat_bytes, hipMemcpyDeviceToDevice, c.st), "feature reference");
     for (int l = 0; l < c.L; ++l) {
       // keys and values [slot, head, token, d]: into the cache from block P
       // on; the scoring block's values go to the scoring reference (as a
@@ -521,11 +537,13 @@ mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0, in
       void* vcopy = l == score_layer && l >= c.P ? vref : nullptr;
       s = dense_block(c, l, l == 0, x, kd, vd, vcopy, l == c.L - 1 ? Yslot : nullptr);
       if (s != MAR_OK) return s;
+      if (features && l == c.P - 1)
+        STEP_HIP(hipMemcpyAsync(fref, hbuf, feat_bytes, hipMemcpyDeviceToDevice, c.st), "feature reference");
     }
     for (int b = slot0; b < slot0 + n_slots; ++b) cache->filled[b] = 1;
   } else {
     const int Mfull = n_slots * S;
-    if (c.P == 0) {
+    if (c.P == 0 && !features) {
       // score pass: value rows of block 0 from x
       const LayerPtrs& w = cache->layers[0];
       void* a = cache->at<void>(lay.a);
@@ -557,8 +575,16 @@ mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0, in
     }
     double* scores = cache->at<double>(lay.scores);
     int32_t* idx = cache->at<int32_t>(lay.idx);
-    TIMED(MAR_PROF_SCORES, 0, 3.0 * Mfull * c.D * c.es + 8.0 * Mfull,
-          launch_scores(c.dtype, vcur, vref, n_slots, c.H, S, c.dh, scores, true, c.st), "scores");
+    if (features) {
+      // a feature row is one "head" of width D in the scoring layout
+      TIMED(MAR_PROF_SCORES, 0, 3.0 * Mfull * c.D * static_cast<double>(fes) + 8.0 * Mfull,
+            launch_scores(c.P == 0 ? c.dtype : static_cast<int>(DT_F32), c.P == 0 ? x : hbuf, fref, n_slots,
+                          1, S, c.D, scores, true, c.st),
+            "feature scores");
+    } else {
+      TIMED(MAR_PROF_SCORES, 0, 3.0 * Mfull * c.D * c.es + 8.0 * Mfull,
+            launch_scores(c.dtype, vcur, vref, n_slots, c.H, S, c.dh, scores, true, c.st), "scores");
+    }
     if (mode == MAR_TOKEN_CACHED || mode == MAR_TOKEN_CACHED_MOST_SIMILAR) {
       TIMED(MAR_PROF_SELECT, 0, 8.0 * Mfull + 4.0 * n_slots * N,
             launch_select(scores, n_slots, S, N, mode == MAR_TOKEN_CACHED_MOST_SIMILAR, idx, c.st), "select");
@@ -569,6 +595,33 @@ mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0, in
     } else if (N > 0) {
       STEP_HIP(hipMemcpyAsync(idx, sel_idx, sizeof(int32_t) * n_slots * N, hipMemcpyHostToDevice, c.st),
                "index upload");
+    }
+    if (d.fresh_kv) {
+      // keys/values of every row at block P from this step's block P-1
+      // output (x when P = 0), before the computed rows replace their own
+      const LayerPtrs& w = cache->layers[c.P];
+      const bool from_x = c.P == 0;
+      void* a = cache->at<void>(lay.a);
+      TIMED(MAR_PROF_LAYERNORM, 0, static_cast<double>(Mfull) * c.D * ((from_x ? c.es : 4.0) + c.es),
+            launch_layernorm(c.dtype, from_x ? x : static_cast<const void*>(hbuf), !from_x, nullptr, S, S, Mfull,
+                             c.D, w.ln1_w, w.ln1_b, c.eps, nullptr, a, c.st),
+            "layernorm (fresh keys/values)");
+      EpiArgs e{};
+      e.kind = EPI_QKV;
+      e.bias = w.qkv_b + c.D;
+      e.out = nullptr;
+      e.n_offset = c.D;
+      e.d_model = c.D;
+      e.n_heads = c.H;
+      e.d_head = c.dh;
+      e.seq = S;
+      e.per_slot = S;
+      e.k_cache = offset<void>(w.kc, slot_off, c.es);
+      e.v_cache = offset<void>(w.vc, slot_off, c.es);
+      const void* wkv = offset<const void>(w.qkv_w, static_cast<long>(c.D) * c.D, c.es);
+      TIMED(MAR_PROF_QKV, 2.0 * Mfull * 2 * c.D * c.D,
+            gemm_bytes(Mfull, 2 * c.D, c.D, static_cast<double>(c.es), static_cast<double>(c.es), false),
+            launch_gemm(c.dtype, a, wkv, Mfull, 2 * c.D, c.D, e, c.st), "key/value gemm (fresh)");
     }
     if (N > 0) {
       const int Msel = n_slots * N;

@@ -58,6 +58,11 @@ class MarDims:
     full_prefix: int  # P: blocks always computed on every row (paper: 3)
     dtype: str = "bf16"
     ln_eps: float = 1e-6
+    # method options (Sec. 4.4 alternatives): what the similarity compares
+    # ("values": the paper's choice, or "features"), and whether the
+    # keys/values of the rows not computed are recomputed at block P
+    score_source: str = "values"
+    fresh_kv: bool = False
 
     @property
     def d_head(self) -> int:

@@ -146,6 +146,34 @@ def test_most_similar_rule_matches_oracle(name):
     np.testing.assert_allclose(_host(y), yo, **TOL[dims.dtype])
 
 
+@pytest.mark.parametrize("name", ["bf16-stack-P2", "f32-stack-P1", "bf16-P0", "f32-block-P0"])
+@pytest.mark.parametrize("option", ["features", "fresh_kv", "both"])
+def test_method_options_match_oracle(name, option):
+    """Sec. 4.4 alternatives: scoring the features instead of the value rows,
+    and recomputing every row's keys/values at block P.  Two cached steps
+    after a fill (the second scores against the first's reference)."""
+    from dataclasses import replace
+    dims = replace(SMALL[name], score_source="features" if option in ("features", "both") else "values",
+                   fresh_kv=option in ("fresh_kv", "both"))
+    n = max(1, dims.seq_len // 4)
+    W, cache = _make(dims)
+    x, prev, changed = _gap_inputs(dims, dims.max_slots, n)
+    x2, _, changed2 = _gap_inputs(dims, dims.max_slots, n, seed=31)
+    # the second step differs from the first on its own n rows
+    for b in range(dims.max_slots):
+        keep = np.setdiff1d(np.arange(dims.seq_len), changed2[b])
+        x2[b, keep] = x[b, keep]
+    orc = O.MarOracle(dims, W)
+    _step(cache, prev, B.MAR_FULL)
+    orc.full(prev)
+    for xs, ch in ((x, changed), (x2, changed2)):
+        y, idx = _step(cache, xs, B.MAR_TOKEN_CACHED, n)
+        yo, idxo, _ = orc.cached(xs, n)
+        np.testing.assert_array_equal(idxo, np.sort(ch, axis=1))  # well conditioned
+        np.testing.assert_array_equal(idx, idxo)
+        np.testing.assert_allclose(_host(y), yo, **TOL[dims.dtype])
+
+
 @pytest.mark.parametrize("compute", ["decoded", "undecoded"])
 def test_token_type_rule_through_given_rows(compute):
     """Table 3's token-type strategies: the host rule picks the rows from the

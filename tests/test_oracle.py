@@ -322,6 +322,52 @@ def test_zero_recompute_returns_cache_and_updates_reference():
     assert np.all(s == 1.0)
 
 
+def test_feature_scores_without_prefix_are_the_input_cosines():
+    """score_source = features, no always-computed block: the similarity is
+    the cosine of the stored step inputs themselves."""
+    from dataclasses import replace
+    d = replace(MarDims(3, 32, 4, 128, 12, 2, 0, "bf16"), score_source="features")
+    W, o, x, prev = _setup(d)
+    o.full(prev)
+    _, idx, s = o.cached(x, 5)
+    for b in range(2):
+        np.testing.assert_array_equal(s[b], cosine_scores(x[b], prev[b]))
+        np.testing.assert_array_equal(idx[b], select_least_similar(s[b], 5))
+
+
+@pytest.mark.parametrize("P", [0, 1, 2])
+def test_feature_scores_of_unchanged_input_are_one(P):
+    from dataclasses import replace
+    d = replace(MarDims(3, 32, 4, 128, 12, 2, P, "f32"), score_source="features")
+    W, o, x, _ = _setup(d)
+    y_full = o.full(x)
+    y, idx, s = o.cached(x, 4)
+    assert np.all(s == 1.0)
+    np.testing.assert_array_equal(idx, np.tile(np.arange(4), (2, 1)))
+    np.testing.assert_allclose(y, y_full, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("P", [0, 1, 2])
+def test_fresh_kv_makes_the_first_cached_block_exact(P):
+    """fresh_kv: with one cached block, every computed row sees this step's
+    keys/values of all rows, so its output is the full forward's row; with
+    the cached keys/values (the default) it is not."""
+    from dataclasses import replace
+    base = MarDims(P + 1, 32, 4, 128, 12, 2, P, "f32")
+    for fresh in (True, False):
+        d = replace(base, fresh_kv=fresh)
+        W, o, x, prev = _setup(d)
+        o.full(prev)
+        y, idx, _ = o.cached(x, 5)
+        ref = MarOracle(d, W).full(x)
+        for b in range(2):
+            err = np.abs(y[b][idx[b]] - ref[b][idx[b]]).max()
+            if fresh:
+                assert err < 1e-12
+            else:
+                assert err > 1e-6
+
+
 def test_cached_rows_are_copies_and_selection_ignores_later_blocks():
     d = MarDims(4, 32, 4, 128, 12, 2, 2, "f32")
     W, o, x, prev = _setup(d)
