@@ -10,6 +10,10 @@ alternating conditional-only steps that reuse the stored guidance residual
 with two-pathway steps that store a fresh one; every step ends with the
 guidance combine.  Inputs of all 64 steps are resident in HBM before timing.
 
+--schedule 32 runs the paper's other setting instead (32 decoding steps,
+caching from the 4th step with tau = 5, about 250 of 320 tokens skipped per
+cached step, so N = 70).
+
 Prints one JSON line.  --gpus N with N > 1 exits: this build runs on one GPU.
 """
 from __future__ import annotations
@@ -37,7 +41,8 @@ def parse():
     ap.add_argument("--profile-kind", default="fc1",
                     help="kernel class timed with HIP events for the roofline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--decode-steps", type=int, default=64)
+    ap.add_argument("--schedule", default="64", choices=list(SCHEDULES),
+                    help="the paper's settings: 64 decoding steps (start 5, tau 9) or 32 (start 4, tau 5)")
     ap.add_argument("--score-source", default="values", choices=["values", "features"],
                     help="what the similarity compares (Sec. 4.4): block P-1's value rows or its output features")
     ap.add_argument("--fresh-kv", action="store_true",
@@ -71,8 +76,8 @@ def calibrate_copy():
     print(json.dumps({"copy_bytes": COPY_BYTES, "dispatches": 3}), flush=True)
 
 
-def fc1_shapes(decode_steps: int):
-    """The fc1 products of one schedule: rows M -> launches.  Full steps run
+def fc1_shapes():
+    """The fc1 products of one 64-step MAR-L schedule: rows M -> launches.  Full steps run
     every block on every row of both pathways; cached steps the prefix
     blocks on every row and the rest on N rows per sequence."""
     import torch
@@ -84,7 +89,8 @@ def fc1_shapes(decode_steps: int):
     wl = WORKLOADS["mar-l"]
     d, n, img = wl.dims, wl.n_recompute, wl.images
     counts = {}
-    for p in sch.lazymar_schedule(decode_steps, 5, 9, "alternate"):
+    n_steps, start, tau, _ = SCHEDULES["64"]
+    for p in sch.lazymar_schedule(n_steps, start, tau, "alternate"):
         seqs = 2 * img if (p.mode == sch.FULL or p.branches == sch.BOTH) else img
         if p.mode == sch.FULL:
             counts[seqs * d.seq_len] = counts.get(seqs * d.seq_len, 0) + d.n_layers
@@ -157,6 +163,11 @@ def cpu_baseline(dims, W, recipe, n, plans):
     }
 
 
+# the paper's two settings (Sec. 5.1): decoding steps, first cached step,
+# refresh period tau, and tokens skipped per cached step at 320 tokens
+# (None: the workload's own N)
+SCHEDULES = {"64": (64, 5, 9, None), "32": (32, 4, 5, 250)}
+
 # token-selection rules of the cached steps (Table 3's strategies)
 RULES = {
     "least": "least similar computed (strategy V, LazyMAR)",
@@ -203,7 +214,7 @@ def main():
         calibrate_copy()
         return
     if args.fc1_shapes:
-        fc1_shapes(args.decode_steps)
+        fc1_shapes()
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -231,10 +242,15 @@ def main():
     cache = B.MarCache(dims, blocks, device=dev)
     torch.cuda.synchronize()
     del blocks
-    recipe = decode_recipe(dims, images, args.decode_steps)
-    X = step_inputs_device(recipe, range(args.decode_steps), device=dev)
+    n_steps, start, tau, skipped = SCHEDULES[args.schedule]
+    if skipped is not None:
+        if dims.seq_len != 320:
+            raise SystemExit("the 32-step setting is stated for 320-token sequences")
+        n = dims.seq_len - skipped
+    recipe = decode_recipe(dims, images, n_steps)
+    X = step_inputs_device(recipe, range(n_steps), device=dev)
     cfg_rule = "paper" if args.workload == "mar-l-hires" else "alternate"
-    plans = sch.lazymar_schedule(args.decode_steps, 5, 9, cfg_rule)
+    plans = sch.lazymar_schedule(n_steps, start, tau, cfg_rule)
     Y = cache.output()
     guided = torch.empty((images, dims.seq_len, dims.d_model), dtype=torch.float32, device=dev)
     scale = 4.0
@@ -309,16 +325,16 @@ def main():
         "bytes_per_launch": prof_bytes / max(prof_n, 1),
     }
     line = {
-        "metric": "cached MAR step tokens/s (MAR-L, 64x2 CFG, 64-step LazyMAR schedule)",
+        "metric": f"cached MAR step tokens/s (MAR-L, 64x2 CFG, {n_steps}-step LazyMAR schedule)",
         "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms_per_sched, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": dims.dtype, "data": "synthetic",
         "config": {"workload": wl.name, "images": images, "seq_len": dims.seq_len,
                    "n_recompute": n, "decode_steps": len(plans),
-                   "schedule": "start 5, tau 9, " + cfg_rule + " guidance reuse",
+                   "schedule": f"start {start}, tau {tau}, " + cfg_rule + " guidance reuse",
                    "selection": RULES[args.rule],
                    "score_source": args.score_source, "fresh_kv": args.fresh_kv,
-                   "step": "one 64-decoding-step schedule"},
+                   "step": f"one {n_steps}-decoding-step schedule"},
         "tflops": sched_flops / (ms_per_sched / 1e3) / 1e12,
         "step_ms": mean,
         "speedup_vs_full_recompute": full_sched_ms / ms_per_sched if mean["full"] else None,

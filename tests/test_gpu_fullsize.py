@@ -83,7 +83,9 @@ def _step(cache, x, mode, n=0, slot0=0):
 PLANS = {
     "block-f32": [WORKLOADS["block-f32"].n_recompute],
     "mar-b": [WORKLOADS["mar-b"].n_recompute],
-    "mar-l": [WORKLOADS["mar-l"].n_recompute] * 2,
+    # N = 50 (the 64-step setting), then N = 70 (the 32-step setting: about
+    # 250 of 320 tokens skipped)
+    "mar-l": [WORKLOADS["mar-l"].n_recompute, 70],
     "mar-h": list(MAR_H_SWEEP),
     "mar-l-hires": [WORKLOADS["mar-l-hires"].n_recompute],
 }
