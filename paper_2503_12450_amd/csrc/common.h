@@ -83,12 +83,25 @@ __device__ __forceinline__ int div_by(int m, uint32_t magic, int shift) {
   return magic ? static_cast<int>(__umulhi(static_cast<uint32_t>(m), magic) >> shift) : m;
 }
 
-// Butterfly sums across the 64 lanes of a wave; every lane gets the total.
-// The order of additions is fixed, so the result is deterministic.
+// Sum across the 64 lanes of a wave; every lane gets the total.  Within each
+// row of 16 lanes, four DPP steps (lane swaps 1 and 2 in a quad, then the
+// half-row and row mirrors) leave the row's sum in every lane without a trip
+// through LDS; the four row sums are then added in row order.  The order of
+// additions is fixed, so the result is deterministic.
+template <int CTRL>
+__device__ __forceinline__ float dpp_shift_add(float v) {
+  return v + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v = dpp_shift_add<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+  v = dpp_shift_add<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+  v = dpp_shift_add<0x141>(v);  // row_half_mirror
+  v = dpp_shift_add<0x140>(v);  // row_mirror
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return ((r0 + r1) + r2) + r3;
 }
 __device__ __forceinline__ double wave_sum(double v) {
 #pragma unroll

@@ -3,8 +3,9 @@
 // One wave per row.  Each lane holds groups of 8 consecutive elements in
 // registers (16-byte bf16 or 2x16-byte fp32 loads), so the statistics are a
 // two-pass mean / biased variance over values already in registers, summed
-// with a fixed butterfly order (the result of a row never depends on which
-// other rows are in the launch).  As the gather for the cached blocks
+// across the wave in a fixed order (DPP within rows of 16 lanes, then the
+// four row sums; the result of a row never depends on which other rows are
+// in the launch).  As the gather for the cached blocks
 // (Eq. 9: only the computed rows enter blocks P..L-1), row m reads token
 // idx[m] of its slot and the fp32 copy of that row seeds the compact
 // residual stream.
@@ -74,7 +75,8 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const TIn* __restrict__ 
       for (int j = 0; j < 8; ++j) sum += v[i][j];
     }
   }
-  const float mean = wave_sum(sum) / static_cast<float>(D);
+  const float inv_d = 1.0f / static_cast<float>(D);
+  const float mean = wave_sum(sum) * inv_d;
   float sq = 0.f;
 #pragma unroll
   for (int i = 0; i < kLnMaxGroups; ++i) {
@@ -87,8 +89,8 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const TIn* __restrict__ 
       }
     }
   }
-  const float var = wave_sum(sq) / static_cast<float>(D);
-  const float rstd = 1.0f / sqrtf(var + eps);
+  const float var = wave_sum(sq) * inv_d;
+  const float rstd = __builtin_amdgcn_rsqf(var + eps);  // hardware 1/sqrt (about 1 ulp)
 #pragma unroll
   for (int i = 0; i < kLnMaxGroups; ++i) {
     const int g = lane + 64 * i;
