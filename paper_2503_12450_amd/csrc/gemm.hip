@@ -137,7 +137,12 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+constexpr int cmin(int a, int b) { return a < b ? a : b; }
+
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+// A wave has at most 63 such operations outstanding (issue stalls at that
+// count), so a wait for "all but the last N" with N >= 63 is a wait for all
+// but the last 63.
 template <int N>
 __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
@@ -401,6 +406,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   constexpr int REG_IN_A = PERSIST ? A_BYTES / REGION : NW;
   static_assert(PERSIST ? REG_IN_A + B_BYTES / REGION >= NW : NW * REGION <= STAGES * STAGE_BYTES,
                 "epilogue staging space");
+  // vector-memory operations each wave's epilogue issues whatever the
+  // arguments: a store per chunk per output (three for QKV), plus the
+  // residual loads.  The optional outputs and the index loads are left out,
+  // which only makes the waits that count on this number stricter.
+  constexpr int EPI_IT = HS * (EC * OSZ / 16) / 64;
+  constexpr int EPI_STRIPS = TM * (TN / (EC / 32)) * (32 / HS);
+  constexpr int EPI_OPS = EPI_STRIPS * EPI_IT * (KIND == EPI_RESIDUAL ? 2 : KIND == EPI_QKV ? 3 : 1);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -579,14 +591,25 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     for (int kt = 0; kt < KT; ++kt) {
       // every wave's slice kt has landed once each wave has waited for its
-      // own loads of it: loads complete in issue order, so it waits until
-      // only the loads issued after them remain (one load group per slice,
-      // plus at most one bias load, which only makes the wait stricter)
+      // own loads of it: vector-memory operations complete in issue order,
+      // so it waits until only the operations issued after them remain (one
+      // load group per slice, plus at most one bias load, which only makes
+      // the wait stricter).  The first slices of a later tile were issued
+      // before the previous tile's epilogue, whose stores then need not
+      // complete before the tile starts multiplying.
+      // (without early free slices 0..AHEAD-1; with it only slice 0, as
+      // slice 1 goes out after the epilogue)
+      const bool after_epi = PERSIST && it > 0 && kt < (EF ? 1 : AHEAD);
       if constexpr (EF) {
-        if (kt + 1 < KT || has_next) wait_vm<LOADS>();  // slice kt+1 was issued after slice kt
-        else wait_vm<0>();
+        if (kt + 1 < KT || has_next) {
+          if (after_epi) wait_vm<cmin(LOADS + EPI_OPS, 63)>();
+          else wait_vm<LOADS>();  // slice kt+1 was issued after slice kt
+        } else {
+          wait_vm<0>();
+        }
       } else {
-        wait_vm<LOADS * (STAGES - 2)>();
+        if (after_epi) wait_vm<cmin(LOADS * (STAGES - 2) + EPI_OPS, 63)>();
+        else wait_vm<LOADS * (STAGES - 2)>();
       }
       __builtin_amdgcn_s_barrier();
       // without early free, the stage of slice kt-1 is free (every wave
