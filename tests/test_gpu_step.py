@@ -244,6 +244,39 @@ def test_full_recompute_ratio_is_bitwise_full(name):
     assert torch.equal(y, y_ref)
 
 
+OPTIONS = {"values": {}, "features": dict(score_source="features"), "fresh_kv": dict(fresh_kv=True),
+           "both": dict(score_source="features", fresh_kv=True)}
+RANKED = {"least": B.MAR_TOKEN_CACHED, "most": B.MAR_TOKEN_CACHED_MOST_SIMILAR}
+
+
+@pytest.mark.parametrize("name", ["bf16-stack-P2", "f32-block-P0", "bf16-P0"])
+@pytest.mark.parametrize("option", list(OPTIONS))
+@pytest.mark.parametrize("rule", list(RANKED))
+def test_invariants_hold_for_every_rule_and_option(name, option, rule):
+    """With an unchanged input every score is exactly 1 under both sources,
+    so both rankings break the tie by index and compute rows 0..n-1, and the
+    step equals the full step bit for bit for any n; computing every row
+    equals the full step too (fresh keys/values included: the key/value
+    product visits k in the same order); n = 0 returns the output cache."""
+    from dataclasses import replace
+    dims = replace(SMALL[name], **OPTIONS[option])
+    mode = RANKED[rule]
+    W, cache = _make(dims)
+    _, cache2 = _make(dims)
+    x = normal_rows((dims.max_slots, dims.seq_len, dims.d_model), seed=12, dtype=dims.dtype)
+    y_full, _ = _step(cache, x, B.MAR_FULL)
+    for n in (0, 1, dims.seq_len // 3, dims.seq_len):
+        y, idx = _step(cache, x, mode, n)
+        assert torch.equal(y, y_full), n
+        np.testing.assert_array_equal(idx, np.tile(np.arange(n), (dims.max_slots, 1)))
+    x2 = perturbed(x, seed=13, std=0.5, dtype=dims.dtype)
+    y_all, _ = _step(cache, x2, mode, dims.seq_len)
+    y_ref, _ = _step(cache2, x2, B.MAR_FULL)
+    assert torch.equal(y_all, y_ref)
+    y0, idx0 = _step(cache, x, mode, 0)
+    assert torch.equal(y0, y_all) and idx0.shape == (dims.max_slots, 0)
+
+
 def test_zero_recompute_returns_cache_and_updates_reference():
     dims = SMALL["bf16-stack-P2"]
     W, cache = _make(dims)

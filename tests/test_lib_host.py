@@ -67,3 +67,26 @@ def test_host_checks_run_before_any_device_call():
     assert lib.mar_k_attention(1, 16, 16, 16, 16, 1, 1, 8, 24, 8, None) == B.MAR_E_SHAPE
     assert lib.mar_cache_destroy(None) == B.MAR_OK
     assert lib.mar_output(None) is None
+
+
+@pytest.mark.parametrize("field,value", [("score_source", 2), ("score_source", -1), ("fresh_kv", 2),
+                                         ("fresh_kv", -1)])
+def test_workspace_rejects_unknown_method_options(field, value):
+    lib = B.load()
+    d = B.dims_c(WORKLOADS["block-f32"].dims)
+    setattr(d, field, value)
+    assert lib.mar_workspace_bytes(ctypes.byref(d)) == 0
+    assert field.encode() in lib.mar_last_error()
+
+
+def test_feature_reference_is_sized_by_its_precision():
+    """The feature score source keeps one reference row per token: the step
+    input's storage type when no block is always computed, else the fp32
+    residual stream; the value source needs no such buffer."""
+    from dataclasses import replace
+    for P, dtype, es in ((0, "bf16", 2), (2, "bf16", 4), (0, "f32", 4)):
+        d = MarDims(4, 256, 4, 1024, 64, 3, P, dtype)
+        extra = B.workspace_bytes(replace(d, score_source="features")) - B.workspace_bytes(d)
+        need = d.max_slots * d.seq_len * d.d_model * es
+        assert need <= extra < need + 1024, (P, dtype)
+        assert B.workspace_bytes(replace(d, fresh_kv=True)) == B.workspace_bytes(d)
