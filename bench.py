@@ -14,7 +14,7 @@ guidance combine.  Inputs of all 64 steps are resident in HBM before timing.
 caching from the 4th step with tau = 5, about 250 of 320 tokens skipped per
 cached step, so N = 70).
 
-Prints one JSON line.  --gpus N with N > 1 exits: this build runs on one GPU.
+Prints one JSON line.  --gpus N with N > 1 exits: the measurement is one GPU's share of the work.
 """
 from __future__ import annotations
 
@@ -219,7 +219,8 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: the cached step shards over images with no "
-              "communication, and this build measures one GPU's share (see DESIGN.md).", file=sys.stderr)
+              "communication, so N GPUs each run this workload on 1/N of the images; the "
+              "measurement is one GPU's share.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
