@@ -31,7 +31,8 @@ extern "C" {
  *   copy_f32[m] = r (nullable)
  * with r the source row of m: src is [slots, seq, d] (fp32 if src_f32 else
  * dtype), m < `m`.  Statistics in fp32, biased variance.  d % 8 == 0,
- * d <= 2048. */
+ * d <= 2048; src, w, b, out and copy_f32 16-byte aligned (MAR_E_ARG
+ * otherwise). */
 mar_status mar_k_layernorm(int32_t dtype, const void* src, int32_t src_f32, const int32_t* idx,
                            int32_t per_slot, int32_t seq, int32_t m, int32_t d, const float* w,
                            const float* b, float eps, float* copy_f32, void* out, void* stream);

@@ -732,7 +732,7 @@ mar_status mar_k_layernorm(int32_t dtype, const void* src, int32_t src_f32, cons
   if (!src || !w || !b || !out) return fail(MAR_E_ARG, "NULL pointer");
   if (m < 0 || d < 8 || d % 8 || d > kMaxModel) return fail(MAR_E_SHAPE, "d must be a multiple of 8, <= %d", kMaxModel);
   if (per_slot < 1 || seq < 1 || (!idx && per_slot != seq)) return fail(MAR_E_SHAPE, "bad row mapping");
-  if (!aligned16(src) || !aligned16(out) || (copy_f32 && !aligned16(copy_f32)))
+  if (!aligned16(src) || !aligned16(out) || !aligned16(w) || !aligned16(b) || (copy_f32 && !aligned16(copy_f32)))
     return fail(MAR_E_ARG, "buffers must be 16-byte aligned");
   MAR_HIP(launch_layernorm(dtype, src, src_f32 != 0, idx, per_slot, seq, m, d, w, b, eps, copy_f32, out,
                            static_cast<hipStream_t>(stream)),

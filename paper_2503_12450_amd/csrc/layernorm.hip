@@ -13,8 +13,6 @@
 
 namespace marcache {
 
-constexpr int kLnMaxGroups = 4;  // 4 groups x 8 elements x 64 lanes: D <= 2048
-
 template <typename TIn>
 __device__ __forceinline__ void load8(const TIn* p, float* v);
 template <>
@@ -49,7 +47,11 @@ __device__ __forceinline__ void store8<bf16_t>(bf16_t* p, const float* v) {
   *reinterpret_cast<u32x4_t*>(p) = a;
 }
 
-template <typename TIn, typename TOut>
+// G = groups of 8 elements per lane (D <= 512 G), a template parameter so
+// that the row, the weight and the bias occupy exactly the registers they
+// need.  The weight and bias are loaded with the row, before the first
+// reduction, so their latency hides under the row's.
+template <typename TIn, typename TOut, int G>
 __global__ __launch_bounds__(256) void layernorm_kernel(const TIn* __restrict__ src,
                                                         const int32_t* __restrict__ idx,
                                                         int per_slot, int seq, int M, int D,
@@ -64,13 +66,25 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const TIn* __restrict__ 
   const long tok = idx ? static_cast<long>(idx[m]) : (m - slot * per_slot);
   const TIn* row = src + (slot * seq + tok) * D;
   const int groups = D / 8;
-  float v[kLnMaxGroups][8];
-  float sum = 0.f;
+  float v[G][8], wv[G][8], bv[G][8];
 #pragma unroll
-  for (int i = 0; i < kLnMaxGroups; ++i) {
+  for (int i = 0; i < G; ++i) {
+    const int g = lane + 64 * i;
+    if (g < groups) load8<TIn>(row + g * 8, v[i]);
+  }
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
     const int g = lane + 64 * i;
     if (g < groups) {
-      load8<TIn>(row + g * 8, v[i]);
+      load8<float>(w + g * 8, wv[i]);
+      load8<float>(bias + g * 8, bv[i]);
+    }
+  }
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    const int g = lane + 64 * i;
+    if (g < groups) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) sum += v[i][j];
     }
@@ -79,7 +93,7 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const TIn* __restrict__ 
   const float mean = wave_sum(sum) * inv_d;
   float sq = 0.f;
 #pragma unroll
-  for (int i = 0; i < kLnMaxGroups; ++i) {
+  for (int i = 0; i < G; ++i) {
     const int g = lane + 64 * i;
     if (g < groups) {
 #pragma unroll
@@ -92,30 +106,40 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const TIn* __restrict__ 
   const float var = wave_sum(sq) * inv_d;
   const float rstd = __builtin_amdgcn_rsqf(var + eps);  // hardware 1/sqrt (about 1 ulp)
 #pragma unroll
-  for (int i = 0; i < kLnMaxGroups; ++i) {
+  for (int i = 0; i < G; ++i) {
     const int g = lane + 64 * i;
     if (g < groups) {
       if (copy_f32) store8<float>(copy_f32 + m * D + g * 8, v[i]);
       float o[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int e = g * 8 + j;
-        o[j] = (v[i][j] - mean) * rstd * w[e] + bias[e];
-      }
+      for (int j = 0; j < 8; ++j) o[j] = (v[i][j] - mean) * rstd * wv[i][j] + bv[i][j];
       store8<TOut>(out + m * D + g * 8, o);
     }
   }
+}
+
+template <typename TIn, typename TOut, int G>
+static hipError_t ln_launch_g(const void* src, const int32_t* idx, int per_slot, int seq, int M,
+                              int D, const float* w, const float* b, float eps, float* copy_f32,
+                              void* out, hipStream_t st) {
+  dim3 grid(static_cast<unsigned>((M + 3) / 4));
+  hipLaunchKernelGGL((layernorm_kernel<TIn, TOut, G>), grid, dim3(256), 0, st,
+                     static_cast<const TIn*>(src), idx, per_slot, seq, M, D, w, b, eps,
+                     copy_f32, static_cast<TOut*>(out));
+  return hipGetLastError();
 }
 
 template <typename TIn, typename TOut>
 static hipError_t ln_launch(const void* src, const int32_t* idx, int per_slot, int seq, int M,
                             int D, const float* w, const float* b, float eps, float* copy_f32,
                             void* out, hipStream_t st) {
-  dim3 grid(static_cast<unsigned>((M + 3) / 4));
-  hipLaunchKernelGGL((layernorm_kernel<TIn, TOut>), grid, dim3(256), 0, st,
-                     static_cast<const TIn*>(src), idx, per_slot, seq, M, D, w, b, eps,
-                     copy_f32, static_cast<TOut*>(out));
-  return hipGetLastError();
+  switch ((D / 8 + 63) / 64) {
+    case 1: return ln_launch_g<TIn, TOut, 1>(src, idx, per_slot, seq, M, D, w, b, eps, copy_f32, out, st);
+    case 2: return ln_launch_g<TIn, TOut, 2>(src, idx, per_slot, seq, M, D, w, b, eps, copy_f32, out, st);
+    case 3: return ln_launch_g<TIn, TOut, 3>(src, idx, per_slot, seq, M, D, w, b, eps, copy_f32, out, st);
+    case 4: return ln_launch_g<TIn, TOut, 4>(src, idx, per_slot, seq, M, D, w, b, eps, copy_f32, out, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_layernorm(int dtype, const void* src, bool src_f32, const int32_t* idx,
