@@ -56,7 +56,8 @@ typedef enum {
   MAR_E_SHAPE = -2,     /* dimensions the kernels do not support */
   MAR_E_STATE = -3,     /* cached step before a full step, reuse before store */
   MAR_E_WORKSPACE = -4, /* workspace too small or misaligned */
-  MAR_E_DEVICE = -5     /* HIP runtime error (launch failure, earlier fault) */
+  MAR_E_DEVICE = -5,    /* HIP runtime error (launch failure, earlier fault) */
+  MAR_E_HOST = -6       /* host memory exhausted (handle or profiler bookkeeping) */
 } mar_status;
 
 /* Storage type of activations, weights and the key/value caches.  Matrix

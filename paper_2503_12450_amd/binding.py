@@ -15,7 +15,7 @@ from typing import Dict, List, Optional, Sequence
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmarcache.so")
 
-MAR_OK, MAR_E_ARG, MAR_E_SHAPE, MAR_E_STATE, MAR_E_WORKSPACE, MAR_E_DEVICE = 0, -1, -2, -3, -4, -5
+MAR_OK, MAR_E_ARG, MAR_E_SHAPE, MAR_E_STATE, MAR_E_WORKSPACE, MAR_E_DEVICE, MAR_E_HOST = 0, -1, -2, -3, -4, -5, -6
 MAR_F32, MAR_BF16 = 0, 1
 MAR_FULL, MAR_TOKEN_CACHED, MAR_TOKEN_GIVEN, MAR_TOKEN_CACHED_MOST_SIMILAR = 0, 1, 2, 3
 MAR_CFG_STORE, MAR_CFG_REUSE = 0, 1
@@ -23,7 +23,7 @@ MAR_SCORE_VALUES, MAR_SCORE_FEATURES = 0, 1
 PROF_KINDS = ("qkv", "proj", "fc1", "fc2", "attention", "layernorm", "scores", "select", "cfg")
 
 STATUS_NAMES = {0: "MAR_OK", -1: "MAR_E_ARG", -2: "MAR_E_SHAPE", -3: "MAR_E_STATE",
-                -4: "MAR_E_WORKSPACE", -5: "MAR_E_DEVICE"}
+                -4: "MAR_E_WORKSPACE", -5: "MAR_E_DEVICE", -6: "MAR_E_HOST"}
 
 # every symbol the headers declare (checked by the CPU tests)
 EXPORTED = (

@@ -5,8 +5,8 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <memory>
 #include <new>
-#include <string>
 #include <vector>
 
 #include "../../include/mar_cache.h"
@@ -17,15 +17,17 @@ using namespace marcache;
 
 namespace {
 
-thread_local std::string g_err;
+// The last error of this thread, in a fixed buffer: reporting an error never
+// allocates, so nothing can throw across the C boundary from here.
+thread_local char g_err[512];
+
+void clear_error() { g_err[0] = '\0'; }
 
 mar_status fail(mar_status s, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof(buf), fmt, ap);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
   va_end(ap);
-  g_err = buf;
   return s;
 }
 
@@ -195,7 +197,12 @@ mar_status timed(mar_cache* h, hipStream_t st, int kind, double flops, double by
       hipEvent_t e;
       hipError_t err = hipEventCreate(&e);
       if (err != hipSuccess) return hip_fail(err, "profiler event");
-      h->events.push_back(e);
+      try {
+        h->events.push_back(e);
+      } catch (const std::bad_alloc&) {
+        (void)hipEventDestroy(e);
+        return fail(MAR_E_HOST, "out of host memory");
+      }
     }
     e0 = h->events[h->ev_used];
     e1 = h->events[h->ev_used + 1];
@@ -369,16 +376,22 @@ mar_status cached_block(const StepCtx& c, int l, int N, const int32_t* idx, floa
 
 extern "C" {
 
-const char* mar_last_error(void) { return g_err.c_str(); }
+const char* mar_last_error(void) { return g_err; }
 
 size_t mar_workspace_bytes(const mar_dims* dims) {
   if (check_dims(dims) != MAR_OK) return 0;
-  return make_layout(*dims).total;
+  try {
+    return make_layout(*dims).total;
+  } catch (const std::bad_alloc&) {
+    fail(MAR_E_HOST, "out of host memory");
+    return 0;
+  }
 }
 
-mar_status mar_cache_init(const mar_dims* dims, const mar_block_weights* blocks, void* workspace,
-                          size_t workspace_bytes, void* stream, mar_cache** out) {
-  g_err.clear();
+namespace {
+
+mar_status cache_init(const mar_dims* dims, const mar_block_weights* blocks, void* workspace,
+                      size_t workspace_bytes, void* stream, mar_cache** out) {
   if (!out) return fail(MAR_E_ARG, "out is NULL");
   *out = nullptr;
   mar_status s = check_dims(dims);
@@ -397,8 +410,8 @@ mar_status mar_cache_init(const mar_dims* dims, const mar_block_weights* blocks,
     for (const void* p : ptrs)
       if (!p) return fail(MAR_E_ARG, "block %d has a NULL parameter pointer", l);
   }
-  mar_cache* h = new (std::nothrow) mar_cache;
-  if (!h) return fail(MAR_E_ARG, "out of host memory");
+  std::unique_ptr<mar_cache> h(new (std::nothrow) mar_cache);
+  if (!h) return fail(MAR_E_HOST, "out of host memory");
   h->d = *dims;
   h->lay = lay;
   h->ws = static_cast<unsigned char*>(workspace);
@@ -436,14 +449,23 @@ mar_status mar_cache_init(const mar_dims* dims, const mar_block_weights* blocks,
         {p.fc1_b, b.fc1_b, F * 4},          {p.fc2_b, b.fc2_b, D * 4}};
     for (const Cp& cp : cps) {
       hipError_t e = hipMemcpyAsync(cp.dst, cp.src, cp.bytes, hipMemcpyDeviceToDevice, st);
-      if (e != hipSuccess) {
-        delete h;
-        return hip_fail(e, "weight copy");
-      }
+      if (e != hipSuccess) return hip_fail(e, "weight copy");
     }
   }
-  *out = h;
+  *out = h.release();
   return MAR_OK;
+}
+
+}  // namespace
+
+mar_status mar_cache_init(const mar_dims* dims, const mar_block_weights* blocks, void* workspace,
+                          size_t workspace_bytes, void* stream, mar_cache** out) {
+  clear_error();
+  try {
+    return cache_init(dims, blocks, workspace, workspace_bytes, stream, out);
+  } catch (const std::bad_alloc&) {
+    return fail(MAR_E_HOST, "out of host memory");
+  }
 }
 
 mar_status mar_cache_destroy(mar_cache* cache) {
@@ -458,7 +480,7 @@ const float* mar_output(const mar_cache* cache) {
 
 mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0, int32_t n_slots,
                     int32_t mode, int32_t n_recompute, int32_t* sel_idx, void* stream) {
-  g_err.clear();
+  clear_error();
   if (!cache) return fail(MAR_E_ARG, "cache is NULL");
   const mar_dims& d = cache->d;
   if (!x) return fail(MAR_E_ARG, "x is NULL");
@@ -646,7 +668,7 @@ mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0, in
 mar_status mar_cfg_combine(mar_cache* cache, const float* y_cond, const float* y_uncond, int32_t pair0,
                            int32_t n_pairs, int32_t op, float scale, float* guided, float* uncond_out,
                            void* stream) {
-  g_err.clear();
+  clear_error();
   if (!cache) return fail(MAR_E_ARG, "cache is NULL");
   if (op != MAR_CFG_STORE && op != MAR_CFG_REUSE) return fail(MAR_E_ARG, "unknown op %d", op);
   if (!y_cond || !guided) return fail(MAR_E_ARG, "y_cond and guided are required");
@@ -682,7 +704,7 @@ mar_status mar_cfg_combine(mar_cache* cache, const float* y_cond, const float* y
 }
 
 mar_status mar_profile_start(mar_cache* cache, int32_t kind) {
-  g_err.clear();
+  clear_error();
   if (!cache) return fail(MAR_E_ARG, "cache is NULL");
   if (kind < 0 || kind >= MAR_PROF_KINDS) return fail(MAR_E_ARG, "unknown kernel class %d", kind);
   cache->prof_kind = kind;
@@ -694,7 +716,7 @@ mar_status mar_profile_start(mar_cache* cache, int32_t kind) {
 
 mar_status mar_profile_stop(mar_cache* cache, double* ms_total, int64_t* launches, double* flops,
                             double* bytes) {
-  g_err.clear();
+  clear_error();
   if (!cache) return fail(MAR_E_ARG, "cache is NULL");
   if (cache->prof_kind < 0) return fail(MAR_E_STATE, "no profile session");
   double total = 0.0;
@@ -727,7 +749,7 @@ static mar_status check_dtype(int32_t dtype) {
 mar_status mar_k_layernorm(int32_t dtype, const void* src, int32_t src_f32, const int32_t* idx,
                            int32_t per_slot, int32_t seq, int32_t m, int32_t d, const float* w,
                            const float* b, float eps, float* copy_f32, void* out, void* stream) {
-  g_err.clear();
+  clear_error();
   if (check_dtype(dtype) != MAR_OK) return MAR_E_ARG;
   if (!src || !w || !b || !out) return fail(MAR_E_ARG, "NULL pointer");
   if (m < 0 || d < 8 || d % 8 || d > kMaxModel) return fail(MAR_E_SHAPE, "d must be a multiple of 8, <= %d", kMaxModel);
@@ -742,7 +764,7 @@ mar_status mar_k_layernorm(int32_t dtype, const void* src, int32_t src_f32, cons
 
 mar_status mar_k_linear(int32_t dtype, int32_t act, const void* a, const void* w, const float* bias,
                         int32_t m, int32_t n, int32_t k, void* out, void* stream) {
-  g_err.clear();
+  clear_error();
   if (check_dtype(dtype) != MAR_OK) return MAR_E_ARG;
   if (!a || !w || !bias || !out) return fail(MAR_E_ARG, "NULL pointer");
   if (m < 0 || k < 64 || k % 64) return fail(MAR_E_SHAPE, "k must be a positive multiple of 64");
@@ -760,7 +782,7 @@ mar_status mar_k_linear_residual(int32_t dtype, const void* a, const void* w, co
                                  int32_t n, int32_t k, const float* resid, float* out,
                                  const int32_t* out_idx, int32_t per_slot, int32_t seq,
                                  float* resid_copy, void* stream) {
-  g_err.clear();
+  clear_error();
   if (check_dtype(dtype) != MAR_OK) return MAR_E_ARG;
   if (!a || !w || !bias || !resid || !out) return fail(MAR_E_ARG, "NULL pointer");
   if (m < 0 || k < 64 || k % 64) return fail(MAR_E_SHAPE, "k must be a positive multiple of 64");
@@ -786,7 +808,7 @@ mar_status mar_k_qkv(int32_t dtype, const void* a, const void* w, const float* b
                      int32_t n_cols, int32_t n_offset, int32_t d_model, int32_t n_heads, int32_t seq,
                      int32_t per_slot, const int32_t* idx, void* q_out, void* k_cache, void* v_cache,
                      void* v_copy, void* stream) {
-  g_err.clear();
+  clear_error();
   if (check_dtype(dtype) != MAR_OK) return MAR_E_ARG;
   if (!a || !w || !bias) return fail(MAR_E_ARG, "NULL pointer");
   if (n_heads < 1 || d_model % 64 || d_model % n_heads || (d_model / n_heads) % 16)
@@ -822,7 +844,7 @@ mar_status mar_k_qkv(int32_t dtype, const void* a, const void* w, const float* b
 mar_status mar_k_attention(int32_t dtype, const void* q, const void* k, const void* v, void* out,
                            int32_t n_slots, int32_t n_heads, int32_t seq, int32_t d_head,
                            int32_t per_slot, void* stream) {
-  g_err.clear();
+  clear_error();
   if (check_dtype(dtype) != MAR_OK) return MAR_E_ARG;
   if (!q || !k || !v || !out) return fail(MAR_E_ARG, "NULL pointer");
   if (n_slots < 0 || n_heads < 1 || seq < 1 || per_slot < 0) return fail(MAR_E_SHAPE, "bad sizes");
@@ -837,7 +859,7 @@ mar_status mar_k_attention(int32_t dtype, const void* q, const void* k, const vo
 
 mar_status mar_k_scores(int32_t dtype, const void* v_cur, void* v_ref, int32_t n_slots, int32_t n_heads,
                         int32_t seq, int32_t d_head, double* scores, int32_t update_ref, void* stream) {
-  g_err.clear();
+  clear_error();
   if (check_dtype(dtype) != MAR_OK) return MAR_E_ARG;
   if (!v_cur || !v_ref || !scores) return fail(MAR_E_ARG, "NULL pointer");
   if (n_slots < 0 || n_heads < 1 || seq < 1 || d_head < 8 || d_head % 8)
@@ -851,7 +873,7 @@ mar_status mar_k_scores(int32_t dtype, const void* v_cur, void* v_ref, int32_t n
 
 static mar_status select_rule(const double* scores, int32_t n_slots, int32_t seq, int32_t n, bool largest,
                               int32_t* idx, void* stream) {
-  g_err.clear();
+  clear_error();
   if (!scores || (!idx && n > 0 && n_slots > 0)) return fail(MAR_E_ARG, "NULL pointer");
   if (n_slots < 0 || seq < 1 || seq > kMaxSeq || n < 0 || n > seq) return fail(MAR_E_SHAPE, "bad sizes");
   MAR_HIP(launch_select(scores, n_slots, seq, n, largest, idx, static_cast<hipStream_t>(stream)), "select");
@@ -869,7 +891,7 @@ mar_status mar_k_select_most_similar(const double* scores, int32_t n_slots, int3
 }
 
 mar_status mar_k_gemm_variant(int32_t variant) {
-  g_err.clear();
+  clear_error();
   if (variant < -1 || variant >= MAR_GEMM_VARIANTS) return fail(MAR_E_ARG, "unknown variant %d", variant);
   set_gemm_variant(variant);
   return MAR_OK;
