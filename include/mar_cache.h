@@ -91,12 +91,6 @@ typedef enum {
   MAR_CFG_REUSE = 1  /* conditional pathway only: u_hat = c + C (Eq. 10) */
 } mar_cfg_op;
 
-/* Shape of a stack of identical pre-LN bidirectional blocks:
- *   h = h + W_o MHA(LN1 h) + b_o ;  h = h + W_2 GELU(W_1 LN2 h + b_1) + b_2
- * with exact-erf GELU, biased-variance LayerNorm, no attention mask.
- * Supported: d_model % n_heads == 0, d_head = d_model / n_heads a multiple
- * of 16 and at most 128, d_model and d_mlp multiples of 64, 1 <= seq_len <=
- * 4096, d_model <= 2048, max_slots >= 1, 0 <= full_prefix < n_layers. */
 /* What the similarity of Eq. (8) compares, step to step (Sec. 4.4). */
 typedef enum {
   MAR_SCORE_VALUES = 0,  /* the self-attention value rows of block P-1 (of
@@ -106,7 +100,13 @@ typedef enum {
                             the step input x when P = 0 */
 } mar_score_source;
 
-/* Zero-initialize, then set the fields: the trailing options default to the
+/* Shape of a stack of identical pre-LN bidirectional blocks:
+ *   h = h + W_o MHA(LN1 h) + b_o ;  h = h + W_2 GELU(W_1 LN2 h + b_1) + b_2
+ * with exact-erf GELU, biased-variance LayerNorm, no attention mask.
+ * Supported: d_model % n_heads == 0, d_head = d_model / n_heads a multiple
+ * of 16 and at most 128, d_model and d_mlp multiples of 64, 1 <= seq_len <=
+ * 4096, d_model <= 2048, max_slots >= 1, 0 <= full_prefix < n_layers.
+ * Zero-initialize, then set the fields: the trailing options default to the
  * paper's method. */
 typedef struct {
   int32_t n_layers;     /* L */

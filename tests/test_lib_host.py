@@ -90,3 +90,25 @@ def test_feature_reference_is_sized_by_its_precision():
         need = d.max_slots * d.seq_len * d.d_model * es
         assert need <= extra < need + 1024, (P, dtype)
         assert B.workspace_bytes(replace(d, fresh_kv=True)) == B.workspace_bytes(d)
+
+
+def test_headers_are_plain_c_and_host_entry_points_answer(tmp_path):
+    """tests/abi_check.c is compiled as C99 against include/*.h only and
+    linked to the library; it checks sizing, option validation and the
+    argument checks that precede any device call."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    B.load()  # the library is built
+    libdir = os.path.dirname(B.LIB_PATH)
+    exe = str(tmp_path / "abi_check")
+    build = subprocess.run([cc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic",
+                            "-I", os.path.join(ROOT, "include"), os.path.join(ROOT, "tests", "abi_check.c"),
+                            "-L", libdir, "-lmarcache", "-Wl,-rpath," + libdir, "-o", exe],
+                           capture_output=True, text=True)
+    assert build.returncode == 0, build.stderr
+    run = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    assert run.returncode == 0, run.stdout + run.stderr
+    assert "abi check: ok" in run.stdout
