@@ -146,7 +146,7 @@ def test_most_similar_rule_matches_oracle(name):
     np.testing.assert_allclose(_host(y), yo, **TOL[dims.dtype])
 
 
-@pytest.mark.parametrize("name", ["bf16-stack-P2", "f32-stack-P1", "bf16-P0", "f32-block-P0"])
+@pytest.mark.parametrize("name", ["bf16-stack-P2", "f32-stack-P1", "bf16-P0", "f32-block-P0", "bf16-dh80-P1"])
 @pytest.mark.parametrize("option", ["features", "fresh_kv", "both"])
 def test_method_options_match_oracle(name, option):
     """Sec. 4.4 alternatives: scoring the features instead of the value rows,
@@ -249,7 +249,7 @@ OPTIONS = {"values": {}, "features": dict(score_source="features"), "fresh_kv": 
 RANKED = {"least": B.MAR_TOKEN_CACHED, "most": B.MAR_TOKEN_CACHED_MOST_SIMILAR}
 
 
-@pytest.mark.parametrize("name", ["bf16-stack-P2", "f32-block-P0", "bf16-P0"])
+@pytest.mark.parametrize("name", ["bf16-stack-P2", "f32-block-P0", "bf16-P0", "bf16-dh80-P1"])
 @pytest.mark.parametrize("option", list(OPTIONS))
 @pytest.mark.parametrize("rule", list(RANKED))
 def test_invariants_hold_for_every_rule_and_option(name, option, rule):
