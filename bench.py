@@ -30,6 +30,18 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+# kernel class -> (what it is, the roof that bounds it)
+KIND_ROOFLINE = {
+    "fc1": ("fc1 product (bf16 MFMA, fp32 accumulate)", "mfma"),
+    "qkv": ("QKV product with the key/value cache scatter (bf16 MFMA)", "mfma"),
+    "proj": ("output projection + residual (bf16 MFMA)", "mfma"),
+    "fc2": ("fc2 product + residual, output-cache scatter at the last block (bf16 MFMA)", "mfma"),
+    "attention": ("attention of the computed queries against all keys (bf16 MFMA)", "mfma"),
+    "layernorm": ("LayerNorm, with the row gather of the cached blocks", "hbm"),
+    "scores": ("similarity of every token (fp64 sums)", "hbm"),
+    "select": ("per-sequence ranking of the scores", "hbm"),
+    "cfg": ("guidance combine with the condition cache", "hbm"),
+}
 
 
 def parse():
@@ -38,7 +50,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=3, help="timed schedules")
     ap.add_argument("--warmup", type=int, default=1, help="untimed schedules")
     ap.add_argument("--workload", default="mar-l", choices=["mar-l", "mar-b", "mar-h", "mar-l-hires"])
-    ap.add_argument("--profile-kind", default="fc1",
+    ap.add_argument("--profile-kind", default="fc1", choices=list(KIND_ROOFLINE),
                     help="kernel class timed with HIP events for the roofline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--schedule", default="64", choices=list(SCHEDULES),
@@ -315,15 +327,19 @@ def main():
             sched_flops += FL.step_flops(dims, (2 if p.branches == sch.BOTH else 1) * images, "cached", n)
     full_sched_ms = len(plans) * mean["full"]
 
-    achieved = prof_flops / (prof_ms / 1e3) / 1e12 if prof_ms > 0 else None
+    tflops = prof_flops / (prof_ms / 1e3) / 1e12 if prof_ms > 0 else None
+    gbs = prof_bytes / (prof_ms / 1e3) / 1e9 if prof_ms > 0 else None
+    what, bound = KIND_ROOFLINE[args.profile_kind]
+    achieved, peak, unit = (tflops, PEAK_BF16_TFLOPS, "TFLOP/s") if bound == "mfma" else (gbs, PEAK_HBM_GBS, "GB/s")
     roofline = {
-        "kernel": f"{args.profile_kind} product (bf16 MFMA, fp32 accumulate)",
-        "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-        "frac": (achieved / PEAK_BF16_TFLOPS) if achieved else None,
+        "kernel": what,
+        "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
+        "frac": (achieved / peak) if achieved else None,
         "traffic": recorded_traffic() if args.profile_kind == "fc1" and args.workload == "mar-l" else None,
         "launches": prof_n, "avg_launch_us": 1e3 * prof_ms / max(prof_n, 1),
         "flops_per_launch": prof_flops / max(prof_n, 1),
         "bytes_per_launch": prof_bytes / max(prof_n, 1),
+        "tflops": tflops, "gbs": gbs,
     }
     line = {
         "metric": f"cached MAR step tokens/s (MAR-L, 64x2 CFG, {n_steps}-step LazyMAR schedule)",
