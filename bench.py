@@ -66,6 +66,9 @@ def parse():
                     help="only run the fc1 product once per shape the 64-step MAR-L schedule "
                          "launches (for hardware-counter runs) and print each shape's launches per "
                          "schedule")
+    ap.add_argument("--attention-shapes", action="store_true",
+                    help="only run the attention once per shape the 64-step MAR-L schedule launches (for "
+                         "hardware-counter runs) and print each shape's launches per schedule")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (the reference "
                          "dispatch that scales the HBM byte counters) and exit")
@@ -118,6 +121,41 @@ def fc1_shapes():
         B.k_linear("bf16", a, w, bias, out, gelu=True)
     torch.cuda.synchronize()
     print(json.dumps({"fc1_rows_to_launches_per_schedule": counts, "n": d.d_mlp, "k": d.d_model}), flush=True)
+
+
+def attention_shapes():
+    """The attention launches of one 64-step MAR-L schedule: (sequences, queries per
+    sequence) -> launches.  Every key/value row of a block takes part; full steps and
+    the prefix blocks of cached steps query all rows, the cached blocks N rows."""
+    import torch
+
+    from paper_2503_12450_amd import binding as B
+    from paper_2503_12450_amd import schedule as sch
+    from paper_2503_12450_amd.workload import WORKLOADS
+
+    wl = WORKLOADS["mar-l"]
+    d, n, img = wl.dims, wl.n_recompute, wl.images
+    S, H, dh = d.seq_len, d.n_heads, d.d_model // d.n_heads
+    counts = {}
+    n_steps, start, tau, _ = SCHEDULES["64"]
+    for p in sch.lazymar_schedule(n_steps, start, tau, "alternate"):
+        seqs = 2 * img if (p.mode == sch.FULL or p.branches == sch.BOTH) else img
+        if p.mode == sch.FULL:
+            counts[(seqs, S)] = counts.get((seqs, S), 0) + d.n_layers
+        else:
+            counts[(seqs, S)] = counts.get((seqs, S), 0) + d.full_prefix
+            counts[(seqs, n)] = counts.get((seqs, n), 0) + d.n_layers - d.full_prefix
+    g = torch.Generator(device="cuda:0").manual_seed(0)
+    for seqs, per in sorted(counts, key=lambda k: -k[0] * k[1]):
+        q = torch.randn(seqs * per, d.d_model, device="cuda:0", generator=g).to(torch.bfloat16)
+        kc = torch.randn(seqs, H, S, dh, device="cuda:0", generator=g).to(torch.bfloat16)
+        vc = torch.randn(seqs, H, S, dh, device="cuda:0", generator=g).to(torch.bfloat16)
+        out = torch.empty_like(q)
+        B.k_attention("bf16", q, kc, vc, out, seqs, H, S, dh, per)
+    torch.cuda.synchronize()
+    shapes = {f"{seqs}x{per}": c for (seqs, per), c in sorted(counts.items(), key=lambda kv: -kv[0][0] * kv[0][1])}
+    print(json.dumps({"attention_shapes_to_launches_per_schedule": shapes, "heads": H, "seq": S, "d_head": dh}),
+          flush=True)
 
 
 def recorded_traffic():
@@ -227,6 +265,9 @@ def main():
         return
     if args.fc1_shapes:
         fc1_shapes()
+        return
+    if args.attention_shapes:
+        attention_shapes()
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
