@@ -73,7 +73,8 @@ def test_layernorm_gather(dtype, src_dtype):
 # --------------------------------------------------------------------------
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (300, 320, 256), (129, 1024, 1024), (1000, 192, 3072)])
+@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (300, 320, 256), (129, 1024, 1024), (1000, 192, 3072),
+                                   (65, 264, 128), (7, 8, 64)])  # columns ending mid-tile, by 8
 @pytest.mark.parametrize("gelu", [False, True])
 def test_linear(dtype, M, N, K, gelu):
     a = normal_rows((M, K), seed=21, dtype=dtype)
@@ -154,8 +155,8 @@ def test_persistent_workgroups_walk_several_tiles(dtype, variant):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_linear_residual_in_place_and_scatter(dtype):
-    M, N, K = 200, 256, 512
+@pytest.mark.parametrize("M,N,K", [(200, 256, 512), (200, 264, 128)])
+def test_linear_residual_in_place_and_scatter(dtype, M, N, K):
     a = normal_rows((M, K), seed=31, dtype=dtype)
     w = normal_rows((N, K), seed=32, std=0.05, dtype=dtype)
     bias = normal_rows((N,), seed=33, std=0.5)
