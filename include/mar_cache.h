@@ -159,8 +159,9 @@ mar_status mar_cache_init(const mar_dims* dims, const mar_block_weights* blocks,
  *               block L-1 for every row (computed rows fresh, the others
  *               from the output cache; Eq. 9).  The same values stay in the
  *               output cache, see mar_output.
- *  mode         mar_mode.  MAR_TOKEN_CACHED / MAR_TOKEN_GIVEN need every slot
- *               of the range filled by an earlier MAR_FULL (else
+ *  mode         mar_mode.  The cached modes (MAR_TOKEN_CACHED,
+ *               MAR_TOKEN_GIVEN, MAR_TOKEN_CACHED_MOST_SIMILAR) need every
+ *               slot of the range filled by an earlier MAR_FULL (else
  *               MAR_E_STATE).
  *  n_recompute  N, rows computed per slot in blocks P..L-1 (0 <= N <= S);
  *               ignored by MAR_FULL.
