@@ -69,6 +69,9 @@ def parse():
     ap.add_argument("--attention-shapes", action="store_true",
                     help="only run the attention once per shape the 64-step MAR-L schedule launches (for "
                          "hardware-counter runs) and print each shape's launches per schedule")
+    ap.add_argument("--memory-shapes", action="store_true",
+                    help="only run the memory-bound kernels (LayerNorm dense and gather, scores, select) once "
+                         "each at the MAR-L schedule's shapes (for hardware-counter runs)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (the reference "
                          "dispatch that scales the HBM byte counters) and exit")
@@ -156,6 +159,48 @@ def attention_shapes():
     shapes = {f"{seqs}x{per}": c for (seqs, per), c in sorted(counts.items(), key=lambda kv: -kv[0][0] * kv[0][1])}
     print(json.dumps({"attention_shapes_to_launches_per_schedule": shapes, "heads": H, "seq": S, "d_head": dh}),
           flush=True)
+
+
+def memory_shapes():
+    """The memory-bound kernels once each at the shapes of the 64-step MAR-L schedule (for
+    hardware-counter runs): the dense LayerNorm (both pathways, fp32 residual stream in, bf16
+    out), the gather LayerNorm of the cached blocks (N rows per sequence, with the fp32 copy of
+    the compact residual stream), the similarity scores with the reference update, and the
+    selection.  Prints each launch's algorithmic bytes."""
+    import torch
+
+    from paper_2503_12450_amd import binding as B
+    from paper_2503_12450_amd.workload import WORKLOADS
+
+    wl = WORKLOADS["mar-l"]
+    d, n, img = wl.dims, wl.n_recompute, wl.images
+    S, D, H = d.seq_len, d.d_model, d.n_heads
+    dh, seqs = D // H, 2 * img
+    dev = "cuda:0"
+    g = torch.Generator(device=dev).manual_seed(0)
+    w = torch.ones(D, device=dev)
+    b = torch.zeros(D, device=dev)
+    launches = []
+    h = torch.randn(seqs * S, D, device=dev, generator=g)
+    out = torch.empty(seqs * S, D, device=dev, dtype=torch.bfloat16)
+    B.k_layernorm("bf16", h, w, b, 1e-6, out)
+    launches.append(("layernorm (dense)", f"{seqs * S} rows", seqs * S * D * (4 + 2)))
+    idx = torch.stack([torch.randperm(S, device=dev, generator=g)[:n].sort().values
+                       for _ in range(seqs)]).to(torch.int32)
+    og = torch.empty(seqs * n, D, device=dev, dtype=torch.bfloat16)
+    cg = torch.empty(seqs * n, D, device=dev)
+    B.k_layernorm("bf16", h, w, b, 1e-6, og, idx=idx, per_slot=n, seq=S, copy_f32=cg)
+    launches.append(("layernorm (gather + fp32 copy)", f"{seqs} x {n} of {S} rows", seqs * n * D * (4 + 2 + 4)))
+    vc = torch.randn(seqs, H, S, dh, device=dev, generator=g).to(torch.bfloat16)
+    vr = torch.randn(seqs, H, S, dh, device=dev, generator=g).to(torch.bfloat16)
+    sc = torch.empty(seqs, S, device=dev, dtype=torch.float64)
+    B.k_scores("bf16", vc, vr, sc, update_ref=True)
+    launches.append(("scores (+ reference update)", f"{seqs} x {S} tokens", 3 * seqs * S * D * 2 + seqs * S * 8))
+    sel = torch.empty(seqs, n, device=dev, dtype=torch.int32)
+    B.k_select(sc, n, sel)
+    launches.append(("select", f"{seqs} x {S} -> {n}", seqs * S * 8 + seqs * n * 4))
+    torch.cuda.synchronize()
+    print(json.dumps({"memory_launches": launches}), flush=True)
 
 
 def recorded_traffic():
@@ -268,6 +313,9 @@ def main():
         return
     if args.attention_shapes:
         attention_shapes()
+        return
+    if args.memory_shapes:
+        memory_shapes()
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
