@@ -39,7 +39,8 @@ mar_status mar_k_layernorm(int32_t dtype, const void* src, int32_t src_f32, cons
 
 /* out[m, n] = act(a w^T + bias) in dtype; a [m, k], w [n, k] (nn.Linear
  * layout), bias [n] fp32; act = exact-erf GELU when `act` != 0 (the block's
- * first MLP product), identity otherwise.  k % 64 == 0, n % 8 == 0. */
+ * first MLP product), identity otherwise.  k % 64 == 0, n % 8 == 0; a, w
+ * and out 16-byte aligned (MAR_E_ARG otherwise). */
 mar_status mar_k_linear(int32_t dtype, int32_t act, const void* a, const void* w, const float* bias,
                         int32_t m, int32_t n, int32_t k, void* out, void* stream);
 
@@ -48,7 +49,8 @@ mar_status mar_k_linear(int32_t dtype, int32_t act, const void* a, const void* w
  * written to out[m, n] (out may equal resid), or, when out_idx is given, to
  * out[(m / per_slot) * seq + out_idx[m], n] (the scatter of the fresh rows
  * into the output cache, Eq. 9) with resid_copy[m, n] = x (nullable).
- * k % 64 == 0, n % 8 == 0. */
+ * k % 64 == 0, n % 8 == 0; a, w, resid, out and resid_copy 16-byte
+ * aligned (MAR_E_ARG otherwise). */
 mar_status mar_k_linear_residual(int32_t dtype, const void* a, const void* w, const float* bias,
                                  int32_t m, int32_t n, int32_t k, const float* resid, float* out,
                                  const int32_t* out_idx, int32_t per_slot, int32_t seq,
@@ -64,7 +66,8 @@ mar_status mar_k_linear_residual(int32_t dtype, const void* a, const void* w, co
  *                     nullable) and v_copy, a second buffer of the same
  *                     layout (nullable); one of them required
  * slot/tok from the row mapping.  d_model % 64 == 0, d_head % 16 == 0,
- * n_offset % 32 == 0, n_cols % 8 == 0. */
+ * n_offset % 32 == 0, n_cols % 8 == 0; every matrix argument 16-byte
+ * aligned (MAR_E_ARG otherwise). */
 mar_status mar_k_qkv(int32_t dtype, const void* a, const void* w, const float* bias, int32_t m,
                      int32_t n_cols, int32_t n_offset, int32_t d_model, int32_t n_heads, int32_t seq,
                      int32_t per_slot, const int32_t* idx, void* q_out, void* k_cache, void* v_cache,
@@ -75,7 +78,8 @@ mar_status mar_k_qkv(int32_t dtype, const void* a, const void* w, const float* b
  * columns h * d_head ...), k and v [n_slots, H, seq, d_head] (the cache
  * layout).  Scale
  * 1/sqrt(d_head); softmax statistics in fp32.  d_head in {16, 32, ..., 128}.
- * per_slot == seq is the dense block; per_slot = N the cached one. */
+ * per_slot == seq is the dense block; per_slot = N the cached one.  q, k,
+ * v and out 16-byte aligned (MAR_E_ARG otherwise). */
 mar_status mar_k_attention(int32_t dtype, const void* q, const void* k, const void* v, void* out,
                            int32_t n_slots, int32_t n_heads, int32_t seq, int32_t d_head,
                            int32_t per_slot, void* stream);
@@ -84,7 +88,8 @@ mar_status mar_k_attention(int32_t dtype, const void* q, const void* k, const vo
  * v_cur and v_ref rows (layout [n_slots, H, seq, d_head]; a token's row is
  * its d_head slices over all heads), products and sums in fp64; 1 if both
  * rows are zero, 0 if one is.  With update_ref != 0, v_ref receives v_cur
- * afterwards.  d_head % 8 == 0. */
+ * afterwards.  d_head % 8 == 0; v_cur and v_ref 16-byte aligned
+ * (MAR_E_ARG otherwise). */
 mar_status mar_k_scores(int32_t dtype, const void* v_cur, void* v_ref, int32_t n_slots, int32_t n_heads,
                         int32_t seq, int32_t d_head, double* scores, int32_t update_ref, void* stream);
 
