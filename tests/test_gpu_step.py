@@ -385,3 +385,47 @@ def test_errors_leave_state_untouched():
     with pytest.raises(B.MarError) as e:
         cache.step(mis, B.MAR_FULL)
     assert e.value.status == B.MAR_E_ARG
+
+
+# --------------------------------------------------------------------------
+# Graph capture: a step is a fixed sequence of launches on the caller's
+# stream with no allocation, so serving loops can capture it once
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("mode", [B.MAR_TOKEN_CACHED, B.MAR_TOKEN_CACHED_MOST_SIMILAR])
+def test_captured_step_replays_like_eager_steps(mode):
+    """A cached step captured in a HIP graph, replayed three times with eager
+    work and synchronisation in between, gives bit for bit what three eager
+    calls give on a twin handle (each replay rescored against the reference
+    the previous one left)."""
+    dims = SMALL["bf16-stack-P2"]
+    n = dims.seq_len // 4
+    W, eager = _make(dims)
+    _, graphed = _make(dims)
+    x, prev, _ = _gap_inputs(dims, dims.max_slots, n)
+    xd = to_device(x, dims.dtype)
+    pd = to_device(prev, dims.dtype)
+    shape = (dims.max_slots, dims.seq_len, dims.d_model)
+    want = []
+    eager.step(pd, B.MAR_FULL)
+    for _ in range(3):
+        y = torch.empty(shape, dtype=torch.float32, device=DEV)
+        sel = torch.empty((dims.max_slots, n), dtype=torch.int32, device=DEV)
+        eager.step(xd, mode, n, y=y, sel_idx=sel)
+        want.append((y, sel))
+    torch.cuda.synchronize()
+
+    graphed.step(pd, B.MAR_FULL)
+    y_g = torch.empty(shape, dtype=torch.float32, device=DEV)
+    sel_g = torch.empty((dims.max_slots, n), dtype=torch.int32, device=DEV)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        graphed.step(xd, mode, n, y=y_g, sel_idx=sel_g)
+    for k in range(3):
+        y_g.fill_(-7.0)  # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(sel_g, want[k][1]), k
+        assert torch.equal(y_g, want[k][0]), k
