@@ -14,6 +14,13 @@ guidance combine.  Inputs of all 64 steps are resident in HBM before timing.
 caching from the 4th step with tau = 5, about 250 of 320 tokens skipped per
 cached step, so N = 70).
 
+Other options: --workload (the MAR-B, MAR-H and 1088-token shapes), --rule
+(the selection strategies of the paper's comparison), --score-source and
+--fresh-kv (the method's variants), --profile-kind (which kernel class the
+roofline reports, against the MFMA or the HBM peak).  --fc1-shapes,
+--attention-shapes, --memory-shapes and --calibrate-copy only run single
+launches for hardware-counter passes.
+
 Prints one JSON line.  --gpus N with N > 1 exits: the measurement is one GPU's share of the work.
 """
 from __future__ import annotations
