@@ -224,7 +224,9 @@ typedef enum {
 
 /* Start timing every launch of kernel class `kind` made by later calls on
  * this handle: a HIP event pair is recorded around each such launch on the
- * call's stream (other classes run untouched).  Restarts an open session. */
+ * call's stream (other classes run untouched).  A session times at most
+ * 262144 launches; later launches of the class run untimed and are not
+ * counted.  Restarts an open session. */
 mar_status mar_profile_start(mar_cache* cache, int32_t kind);
 
 /* End the session: waits for the recorded events and returns the summed

@@ -187,10 +187,14 @@ struct StepCtx {
 
 // Runs `launch`; when the handle profiles `kind`, brackets it with a pair of
 // events on the stream and adds the launch's algorithmic work.
+// A session times at most this many launches (an event pair each); later
+// launches of the class run untimed, so a long session cannot exhaust events.
+constexpr size_t kMaxTimedLaunches = size_t(1) << 18;
+
 template <class F>
 mar_status timed(mar_cache* h, hipStream_t st, int kind, double flops, double bytes, F&& launch,
                  const char* what) {
-  const bool on = h->prof_kind == kind;
+  const bool on = h->prof_kind == kind && h->ev_used / 2 < kMaxTimedLaunches;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (on) {
     while (h->events.size() < h->ev_used + 2) {

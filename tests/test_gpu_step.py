@@ -429,3 +429,26 @@ def test_captured_step_replays_like_eager_steps(mode):
         torch.cuda.synchronize()
         assert torch.equal(sel_g, want[k][1]), k
         assert torch.equal(y_g, want[k][0]), k
+
+
+def test_profiler_counts_the_class_launches_and_their_work():
+    """A session around one full step times exactly the class's launches
+    (fc1: one per block) and sums their algorithmic FLOPs (2 M F D each);
+    stopping without a session is a state error."""
+    dims = SMALL["bf16-stack-P2"]
+    W, cache = _make(dims)
+    x = normal_rows((dims.max_slots, dims.seq_len, dims.d_model), seed=14, dtype=dims.dtype)
+    with pytest.raises(B.MarError) as e:
+        cache.profile_stop()
+    assert e.value.status == B.MAR_E_STATE
+    cache.profile_start("fc1")
+    _step(cache, x, B.MAR_FULL)
+    ms, launches, flops, nbytes = cache.profile_stop()
+    M = dims.max_slots * dims.seq_len
+    assert launches == dims.n_layers
+    assert flops == pytest.approx(dims.n_layers * 2.0 * M * dims.d_mlp * dims.d_model, rel=1e-12)
+    assert ms > 0.0 and nbytes > 0.0
+    # a class that the step does not launch on this path times nothing
+    cache.profile_start("select")
+    _step(cache, x, B.MAR_FULL)
+    assert cache.profile_stop()[1] == 0
