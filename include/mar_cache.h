@@ -105,7 +105,10 @@ typedef enum {
  * with exact-erf GELU, biased-variance LayerNorm, no attention mask.
  * Supported: d_model % n_heads == 0, d_head = d_model / n_heads a multiple
  * of 16 and at most 128, d_model and d_mlp multiples of 64, 1 <= seq_len <=
- * 4096, d_model <= 2048, max_slots >= 1, 0 <= full_prefix < n_layers.
+ * 4096, d_model <= 2048, max_slots >= 1, 0 <= full_prefix < n_layers, and
+ * max_slots * seq_len * max(3 d_model, d_mlp) * 4 < 2^31 (the kernels
+ * address each operand and output with 32-bit byte offsets; MAR-H shapes,
+ * seq_len 320 and d_mlp 5120, allow up to 327 slots).
  * Zero-initialize, then set the fields: the trailing options default to the
  * paper's method. */
 typedef struct {
@@ -194,7 +197,8 @@ mar_status mar_step(mar_cache* cache, const void* x, float* y, int32_t slot0,
  * guided is required; uncond_out (nullable) receives u (STORE) or u_hat
  * (REUSE).  The mix is evaluated as fmaf(scale, c - u, u) in fp32.  REUSE
  * of a pair never stored returns MAR_E_STATE.  Pairs index the residual
- * store, not slots: 0 <= pair0, pair0 + n_pairs <= max_slots. */
+ * store, not slots; the store holds ceil(max_slots / 2) pairs:
+ * 0 <= pair0, pair0 + n_pairs <= (max_slots + 1) / 2. */
 mar_status mar_cfg_combine(mar_cache* cache, const float* y_cond,
                            const float* y_uncond, int32_t pair0, int32_t n_pairs,
                            int32_t op, float scale, float* guided,

@@ -2,6 +2,7 @@
 // the kernel sequence of one step (full, token-cached, or given rows).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -67,6 +68,24 @@ mar_status check_dims(const mar_dims* d) {
   if (d->score_source != MAR_SCORE_VALUES && d->score_source != MAR_SCORE_FEATURES)
     return fail(MAR_E_ARG, "unknown score_source %d", d->score_source);
   if (d->fresh_kv != 0 && d->fresh_kv != 1) return fail(MAR_E_ARG, "fresh_kv must be 0 or 1");
+  // The products address operands and outputs through buffer descriptors
+  // with 32-bit byte offsets (launch_gemm refuses anything that reaches
+  // 2 GiB).  Checked here, so that every step mar_workspace_bytes accepts
+  // runs to the end once its arguments pass: the widest product of a full
+  // step writes max_slots * seq_len rows of max(3 d_model, d_mlp) columns
+  // (fp32-sized in the check); the key/value caches, the output cache and
+  // the residual stream are narrower; a weight panel is 256 rows of K.
+  const size_t es = d->dtype == MAR_BF16 ? 2 : 4;
+  const size_t lim = size_t(1) << 31;
+  const size_t rows = static_cast<size_t>(d->max_slots) * d->seq_len;
+  const size_t widest = std::max<size_t>(3 * static_cast<size_t>(d->d_model), d->d_mlp);
+  if (rows * widest * 4 >= lim)
+    return fail(MAR_E_SHAPE,
+                "max_slots * seq_len * max(3 d_model, d_mlp) * 4 = %zu bytes reaches 2 GiB (32-bit offsets); "
+                "use fewer slots per cache",
+                rows * widest * 4);
+  if (size_t(256) * std::max(d->d_model, d->d_mlp) * es >= lim)
+    return fail(MAR_E_SHAPE, "d_mlp %d too large for 32-bit weight offsets", d->d_mlp);
   return MAR_OK;
 }
 

@@ -51,6 +51,21 @@ int main(void) {
   d.seq_len = 4097;
   CHECK(mar_workspace_bytes(&d) == 0);
   d.seq_len = 320;
+  /* 32-bit offsets: MAR-H shapes fit 327 slots, not 330 (the widest
+   * product, fc1 on every row of a full step, would reach 2 GiB) */
+  d.n_layers = 40;
+  d.d_model = 1280;
+  d.d_mlp = 5120;
+  d.max_slots = 327;
+  CHECK(mar_workspace_bytes(&d) > 0);
+  d.max_slots = 330;
+  CHECK(mar_workspace_bytes(&d) == 0);
+  CHECK(strstr(mar_last_error(), "2 GiB") != NULL);
+  CHECK(mar_cache_init(&d, NULL, NULL, 0, NULL, &h) == MAR_E_SHAPE);
+  d.n_layers = 32;
+  d.d_model = 1024;
+  d.d_mlp = 4096;
+  d.max_slots = 128;
 
   /* argument checks come before any device work */
   CHECK(mar_cache_init(&d, NULL, NULL, 0, NULL, &h) == MAR_E_ARG);

@@ -55,6 +55,25 @@ def test_workspace_rejects_unsupported_dims(bad):
     assert e.value.status == B.MAR_E_SHAPE
 
 
+@pytest.mark.parametrize("slots,ok", [(256, True), (327, True), (328, False), (330, False)])
+def test_workspace_rejects_dims_past_32_bit_offsets(slots, ok):
+    """Every product addresses its operands and outputs with 32-bit byte
+    offsets.  The sizing call refuses any dims for which one launch of a
+    step would pass 2 GiB: fc1 on every row of a full step writes
+    max_slots * seq_len * d_mlp values, counted at 4 bytes.  So no accepted
+    dims can make a step fail after it has started enqueueing work."""
+    from dataclasses import replace
+    d = replace(WORKLOADS["mar-h"].dims, max_slots=slots)
+    assert (d.max_slots * d.seq_len * max(3 * d.d_model, d.d_mlp) * 4 < 2 ** 31) == ok
+    if ok:
+        assert B.workspace_bytes(d) > 0
+        return
+    with pytest.raises(B.MarError) as e:
+        B.workspace_bytes(d)
+    assert e.value.status == B.MAR_E_SHAPE
+    assert "2 GiB" in str(e.value)
+
+
 def test_host_checks_run_before_any_device_call():
     lib = B.load()
     d = B.dims_c(WORKLOADS["block-f32"].dims)
