@@ -259,13 +259,17 @@ def cpu_baseline(dims, W, recipe, n, plans):
     tokens = len(plans) * dims.seq_len
     return {
         "value": tokens / t_sched, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+        "host_cpus": os.cpu_count(), "cpus_available": len(os.sched_getaffinity(0)),
+        "threads_note": (f"the oracle's matrix products ran on {threads} BLAS threads; its other work "
+                         "(the exactly rounded score sums, attention per head, LayerNorm) is single-threaded "
+                         "numpy/Python"),
         "sample": (f"fp64 numpy oracle, one sequence: median of {reps} full steps ({t_full:.2f} s) and of {reps} "
                    f"token-cached steps N={n} ({t_cached:.2f} s) at the {dims.n_layers}-block width-{dims.d_model} "
                    f"shape; one image's schedule composed as {seq_full} full + {seq_cached} cached sequence-steps"),
     }
 
 
-# the paper's two settings (Sec. 5.1): decoding steps, first cached step,
+# the paper's two settings (Sec. 4.1): decoding steps, first cached step,
 # refresh period tau, and tokens skipped per cached step at 320 tokens
 # (None: the workload's own N)
 SCHEDULES = {"64": (64, 5, 9, None), "32": (32, 4, 5, 250)}

@@ -271,6 +271,15 @@ class MarOracle:
     def _score_layer(self) -> int:
         return max(self.P - 1, 0)
 
+    def _block(self, m, rows, l: int):
+        """Block l on the rows ``rows`` of the block input m (one sequence)."""
+        return block_rows(m, rows, self.blocks[l], self.H, self.eps)
+
+    def _values(self, x) -> np.ndarray:
+        """Value rows of block 0 formed from the step input (no always-computed
+        block)."""
+        return value_rows(x, self.blocks[0], self.eps)
+
     def full_slot(self, b: int, x) -> np.ndarray:
         """Full step (refresh / warm-up): every block on every row; fills the
         token cache of every cached block and the scoring reference."""
@@ -281,7 +290,7 @@ class MarOracle:
             hc[-1] = h.copy()
             self.fref[b] = h.copy()
         for l in range(self.L):
-            h, v = block_rows(h, rows, self.blocks[l], self.H, self.eps)
+            h, v = self._block(h, rows, l)
             if l == self._score_layer():
                 self.vref[b] = storage_round(v, self.dtype)
             if l == self.P - 1:
@@ -306,10 +315,10 @@ class MarOracle:
         h = _f64(x).reshape(self.S, self.D)
         rows_all = np.arange(self.S)
         if self.P == 0:
-            v = value_rows(h, self.blocks[0], self.eps)
+            v = self._values(h)
         else:
             for l in range(self.P):
-                h, v = block_rows(h, rows_all, self.blocks[l], self.H, self.eps)
+                h, v = self._block(h, rows_all, l)
         v = storage_round(v, self.dtype)
         if self.score_source == "features":
             feat = h.copy() if self.P == 0 else storage_round(h, "f32")
@@ -330,7 +339,7 @@ class MarOracle:
         fresh = h[idx]
         for l in range(self.P, self.L):
             hc[l - 1][idx] = fresh
-            fresh, _ = block_rows(hc[l - 1], idx, self.blocks[l], self.H, self.eps)
+            fresh, _ = self._block(hc[l - 1], idx, l)
             hc[l][idx] = fresh
         return hc[self.L - 1].copy(), idx, scores
 

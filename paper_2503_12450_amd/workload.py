@@ -215,6 +215,37 @@ def random_index_sets(n_slots: int, seq: int, n: int, seed: int, stream: int = 0
     return out
 
 
+def changed_rows(base: np.ndarray, n: int, seed: int):
+    """A copy of ``base`` [slots, S, D] in which n random rows per slot (the
+    rows of random_index_sets(seed)) get N(0, 1) noise added (normal_rows,
+    seed + 1); not yet rounded to a storage type.  Returns (copy, rows).
+    A cached step on such an input has a well separated selection: the
+    changed rows are far less similar than every other row."""
+    rows = random_index_sets(base.shape[0], base.shape[1], n, seed=seed)
+    noise = normal_rows(base.shape, seed=seed + 1)
+    out = base.copy()
+    for b in range(base.shape[0]):
+        out[b, rows[b]] = base[b, rows[b]] + noise[b, rows[b]]
+    return out, rows
+
+
+# Full-size parity plan: workload -> recompute counts of the successive
+# cached steps after one full step (each step's input from changed_rows with
+# seed 100 + 10 k; then, for two-pathway workloads, one conditional-only
+# step at the last count with seed 900)
+FULLSIZE_PLANS = {
+    "block-f32": (WORKLOADS["block-f32"].n_recompute,),
+    "mar-b": (WORKLOADS["mar-b"].n_recompute,),
+    # N = 50 (the 64-step setting), then N = 70 (the 32-step setting: about
+    # 250 of 320 tokens skipped)
+    "mar-l": (WORKLOADS["mar-l"].n_recompute, 70),
+    "mar-h": MAR_H_SWEEP,
+    "mar-l-hires": (WORKLOADS["mar-l-hires"].n_recompute,),
+}
+FULLSIZE_STEP_SEED = 100
+FULLSIZE_COND_SEED = 900
+
+
 # ---------------------------------------------------------------------------
 # Masked-generation decode schedule inputs (Eq. 6 layout, cosine mask schedule)
 # ---------------------------------------------------------------------------
@@ -334,3 +365,89 @@ def step_inputs_device(recipe: DecodeRecipe, steps, device="cuda"):
         out.append(x.to(tdt).contiguous())
         del x, img, dec
     return out
+
+
+# ---------------------------------------------------------------------------
+# Per-token diffusion head (the denoiser MAR samples each token's latent with)
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class HeadDims:
+    """Shape of the per-token diffusion head: a residual MLP of `depth`
+    blocks and width `width`, conditioned by adaptive LayerNorm on the
+    transformer's output row (cond_dim) and the diffusion time; it predicts
+    the noise of a `token_dim`-dimensional latent.  `steps` sampling steps
+    respace a `train_steps`-step linear noise schedule."""
+
+    width: int
+    depth: int
+    cond_dim: int
+    token_dim: int = LATENT_DIM
+    steps: int = 100
+    train_steps: int = 1000
+    beta_start: float = 1e-4
+    beta_end: float = 0.02
+    freq_dim: int = 256
+    max_rows: int = 4096
+    dtype: str = "bf16"
+    ln_eps: float = 1e-6
+
+    @property
+    def n_mod(self) -> int:
+        """Modulation vectors per row: shift, scale, gate per block, and the
+        final shift and scale."""
+        return 3 * self.depth + 2
+
+
+# Head sizes per model: chosen so that the head's FLOPs over one image (256
+# tokens x 2 guidance pathways x 100 steps) reproduce the step-count
+# independent constant of Table 1's baseline FLOPs within a few percent
+# (checked in the tests).
+HEADS = {
+    "mar-b": HeadDims(width=1024, depth=6, cond_dim=768),
+    "mar-l": HeadDims(width=1280, depth=8, cond_dim=1024),
+    "mar-h": HeadDims(width=1536, depth=12, cond_dim=1280),
+}
+
+HEAD_WEIGHT_NAMES = ("z_w", "z_b", "t1_w", "t1_b", "t2_w", "t2_b", "in_w", "in_b", "ada_w", "ada_b",
+                     "fc1_w", "fc1_b", "fc2_w", "fc2_b", "out_w", "out_b")
+
+
+def head_weights(hd: HeadDims, seed: int = SEED_WEIGHTS, std: float = 0.02) -> Dict[str, np.ndarray]:
+    """Random weights of the head, nn.Linear layout ([out, in]).  Per-block
+    matrices are stacked on a leading axis: fc1_w, fc2_w [depth, w, w],
+    fc1_b, fc2_b [depth, w]; ada_w [n_mod * w, w] holds the modulation
+    products of every block and the final layer, block k's shift, scale and
+    gate at rows (3k, 3k+1, 3k+2) * w, the final shift and scale last.
+    Matrices are rounded to the storage type; biases stay fp32.  The input
+    and output products (token_dim wide) use a larger scale so that the
+    noise prediction is O(1)."""
+    w, D, T = hd.width, hd.cond_dim, hd.token_dim
+    g = _gen(seed, 1000)
+
+    def n(*shape, s=std):
+        return (g.standard_normal(shape, dtype=np.float32) * np.float32(s)).astype(np.float32)
+
+    out = {
+        "z_w": n(w, D), "z_b": n(w),
+        "t1_w": n(w, hd.freq_dim, s=0.1), "t1_b": n(w),
+        "t2_w": n(w, w), "t2_b": n(w),
+        "in_w": n(w, T, s=0.25), "in_b": n(w),
+        "ada_w": n(hd.n_mod * w, w), "ada_b": n(hd.n_mod * w),
+        "fc1_w": n(hd.depth, w, w), "fc1_b": n(hd.depth, w),
+        "fc2_w": n(hd.depth, w, w), "fc2_b": n(hd.depth, w),
+        "out_w": n(T, w, s=1.0 / math.sqrt(w)), "out_b": n(T),
+    }
+    out = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in out.items()}
+    for k in ("z_w", "t1_w", "t2_w", "in_w", "ada_w", "fc1_w", "fc2_w", "out_w"):
+        out[k] = to_storage(out[k], hd.dtype)
+    return out
+
+
+def decoded_at(recipe: "DecodeRecipe", step: int) -> np.ndarray:
+    """int64 [images, n]: the image tokens decoded at decoding step ``step``
+    (the order's entries between the counts before and after it), the same
+    number for every image."""
+    T = recipe.image_tokens
+    lo, hi = T - int(recipe.counts[step]), T - int(recipe.counts[step + 1])
+    return np.sort(recipe.order[:, lo:hi], axis=1)

@@ -4,22 +4,34 @@ launch configuration the benchmark times), checked on sampled sequences.
 The GPU advances every slot of the workload; the oracle follows the same
 steps for a few sampled slots, one sequence at a time (Sec. 3.2 / Eq. 8-9).
 Selected indices must match exactly.  Block outputs: fp32 stacks within
-atol 1e-4 / rtol 1e-5 elementwise; bf16 stacks within max-abs 2e-2 /
-rel 1e-2, where at full depth "rel" is taken relative to the sequence's
-activation scale: max |gpu - oracle| <= max(2e-2, 1e-2 * max |oracle|).
-Rounding every stored bf16 activation exactly (an fp64 emulation of the
-path's storage points) already exceeds the elementwise form of that bar on a
-few elements of a 24-block stack; the shallow-stack tests keep the
-elementwise form.
+atol 1e-4 / rtol 1e-5 elementwise.
+
+bf16 stacks at full depth (24-40 blocks): the bar of max-abs 2e-2 /
+rel 1e-2 (|gpu - oracle| <= 2e-2 + 1e-2 |oracle| per element) cannot hold
+at every element for any pipeline that stores its product operands in
+bfloat16: the oracle itself, rounding every tensor exactly where the path
+stores it and computing everything else exactly (oracle.storage_emulation),
+already moves some elements past it, more with depth.  Those figures are
+stored per check in tests/golden/bf16_storage_error.json (written by the
+script beside it, from oracle/ alone).  The GPU must stay within a small
+multiple of them:
+  max |gpu - oracle| <= 1.25 x the emulation's maximum deviation, and
+  elements beyond the elementwise bar <= 1.25 x the emulation's count
+  + 3 sqrt(count) + 3 (the count of a few rare events is noisy).
+A kernel whose error doubled would fail both.
 
 The selection is made well conditioned the same way as in the small step
 tests: each cached step's input differs from the previous step's on exactly
-N rows per sequence by O(1) noise, so the N least similar rows are far from
-every other row in score on both sides, whatever the rounding of the value
-rows.  A two-pathway workload also takes a conditional-only step
-(slots [0, B)) and the guidance store/reuse on its sampled pair.
+N rows per sequence by O(1) noise (workload.changed_rows), so the N least
+similar rows are far from every other row in score on both sides, whatever
+the rounding of the value rows.  A two-pathway workload also takes a
+conditional-only step (slots [0, B)) and the guidance store/reuse on its
+sampled pair.
 """
 import functools
+import json
+import math
+import os
 
 import numpy as np
 import pytest
@@ -28,24 +40,39 @@ import torch
 import oracle as O
 from paper_2503_12450_amd import binding as B
 from paper_2503_12450_amd.device import to_device, upload_blocks
-from paper_2503_12450_amd.workload import (MAR_H_SWEEP, WORKLOADS, all_block_weights, normal_rows,
-                                           random_index_sets, to_storage)
+from paper_2503_12450_amd.workload import (FULLSIZE_COND_SEED, FULLSIZE_PLANS, FULLSIZE_STEP_SEED, WORKLOADS,
+                                           all_block_weights, changed_rows, normal_rows, to_storage)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
-TOL = {"f32": dict(atol=1e-4, rtol=1e-5), "bf16": dict(atol=2e-2, rtol=1e-2)}
+TOL_F32 = dict(atol=1e-4, rtol=1e-5)
+ATOL, RTOL = 2e-2, 1e-2
+MAX_RATIO = 1.25     # GPU max deviation / storage-rounding max deviation
+COUNT_RATIO = 1.25   # GPU elements beyond the bar / storage-rounding count
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "bf16_storage_error.json")
 
 
-def _close(got, want, dtype, what):
+@functools.lru_cache(maxsize=1)
+def _storage_figures():
+    with open(GOLDEN) as f:
+        return json.load(f)
+
+
+def _close(got, want, dtype, what, name):
     if dtype == "f32":
-        np.testing.assert_allclose(got, want, err_msg=what, **TOL["f32"])
+        np.testing.assert_allclose(got, want, err_msg=what, **TOL_F32)
         return
-    err = float(np.abs(got - want).max())
-    bound = max(2e-2, 1e-2 * float(np.abs(want).max()))
-    strict = int((np.abs(got - want) > 2e-2 + 1e-2 * np.abs(want)).sum())
-    print(f"  {what}: max err {err:.4f} (bound {bound:.4f}); {strict} of {want.size} beyond the elementwise form",
-          flush=True)
-    assert err <= bound, f"{what}: max error {err} > {bound}"
+    ref = _storage_figures()[name][what]
+    e = np.abs(got - want)
+    err = float(e.max())
+    beyond = int((e > ATOL + RTOL * np.abs(want)).sum())
+    max_bound = MAX_RATIO * ref["max_err"]
+    count_bound = COUNT_RATIO * ref["beyond"] + 3.0 * math.sqrt(ref["beyond"]) + 3.0
+    print(f"  {what}: max err {err:.4f} (storage rounding alone {ref['max_err']:.4f}, bound {max_bound:.4f}); "
+          f"{beyond} of {want.size} beyond the elementwise bar (storage rounding alone {ref['beyond']}, "
+          f"bound {count_bound:.0f})", flush=True)
+    assert err <= max_bound, f"{what}: max error {err} > {max_bound}"
+    assert beyond <= count_bound, f"{what}: {beyond} elements beyond the bar > {count_bound}"
 
 
 def _host(t):
@@ -55,17 +82,6 @@ def _host(t):
 @functools.lru_cache(maxsize=1)
 def _weights(name):
     return all_block_weights(WORKLOADS[name].dims)
-
-
-def _changed(base, n, seed):
-    """A copy of base whose rows differ on n random rows per sequence by
-    N(0, 1) noise (not yet rounded to the storage dtype)."""
-    rows = random_index_sets(base.shape[0], base.shape[1], n, seed=seed)
-    noise = normal_rows(base.shape, seed=seed + 1)
-    out = base.copy()
-    for b in range(base.shape[0]):
-        out[b, rows[b]] = base[b, rows[b]] + noise[b, rows[b]]
-    return out, rows
 
 
 def _step(cache, x, mode, n=0, slot0=0):
@@ -79,25 +95,13 @@ def _step(cache, x, mode, n=0, slot0=0):
     return y, (sel[:, :n].cpu().numpy() if sel is not None else None)
 
 
-# workload -> recompute counts of the successive cached steps
-PLANS = {
-    "block-f32": [WORKLOADS["block-f32"].n_recompute],
-    "mar-b": [WORKLOADS["mar-b"].n_recompute],
-    # N = 50 (the 64-step setting), then N = 70 (the 32-step setting: about
-    # 250 of 320 tokens skipped)
-    "mar-l": [WORKLOADS["mar-l"].n_recompute, 70],
-    "mar-h": list(MAR_H_SWEEP),
-    "mar-l-hires": [WORKLOADS["mar-l-hires"].n_recompute],
-}
-
-
-@pytest.mark.parametrize("name", list(PLANS))
+@pytest.mark.parametrize("name", list(FULLSIZE_PLANS))
 def test_full_size_steps_on_sampled_sequences(name):
     wl = WORKLOADS[name]
     dims = wl.dims
     slots = dims.max_slots
     print(f"[fullsize] {name}: {slots} slots x {dims.seq_len} tokens, width {dims.d_model}, "
-          f"{dims.n_layers} blocks, N plan {PLANS[name]}", flush=True)
+          f"{dims.n_layers} blocks, N plan {list(FULLSIZE_PLANS[name])}", flush=True)
     W = _weights(name)
     cache = B.MarCache(dims, upload_blocks(W, dims.dtype))
     sample = sorted({0, slots - 1})
@@ -107,10 +111,10 @@ def test_full_size_steps_on_sampled_sequences(name):
     y, _ = _step(cache, x, B.MAR_FULL)
     yh = _host(y)
     for b in sample:
-        _close(yh[b], orc.full_slot(b, x[b]), dims.dtype, f"full step, slot {b}")
+        _close(yh[b], orc.full_slot(b, x[b]), dims.dtype, f"full step, slot {b}", name)
 
-    for k, n in enumerate(PLANS[name]):
-        nxt, rows = _changed(x, n, seed=100 + 10 * k)
+    for k, n in enumerate(FULLSIZE_PLANS[name]):
+        nxt, rows = changed_rows(x, n, seed=FULLSIZE_STEP_SEED + 10 * k)
         nxt = to_storage(nxt, dims.dtype)
         y, idx = _step(cache, nxt, B.MAR_TOKEN_CACHED, n)
         yh = _host(y)
@@ -118,24 +122,24 @@ def test_full_size_steps_on_sampled_sequences(name):
             yo, idxo, _ = orc.cached_slot(b, nxt[b], n)
             np.testing.assert_array_equal(idx[b], idxo, err_msg=f"selection, step {k}, slot {b}")
             np.testing.assert_array_equal(idxo, np.sort(rows[b]))  # the construction is well conditioned
-            _close(yh[b], yo, dims.dtype, f"cached step {k} (N={n}), slot {b}")
+            _close(yh[b], yo, dims.dtype, f"cached step {k} (N={n}), slot {b}", name)
         x = nxt
 
     if slots >= 2 and slots % 2 == 0 and wl.images:
         # conditional pathway only (slots [0, B)), then guidance with the
         # residual stored from the last two-pathway step
         half = slots // 2
-        n = PLANS[name][-1]
+        n = FULLSIZE_PLANS[name][-1]
         y_both = torch.from_numpy(yh.astype(np.float32)).to(DEV)
         guided = torch.empty((half, dims.seq_len, dims.d_model), dtype=torch.float32, device=DEV)
         cache.cfg_combine(B.MAR_CFG_STORE, y_both[:half], y_both[half:], 4.0, guided)
-        nxt, rows = _changed(x[:half], n, seed=900)
+        nxt, rows = changed_rows(x[:half], n, seed=FULLSIZE_COND_SEED)
         nxt = to_storage(nxt, dims.dtype)
         y, idx = _step(cache, nxt, B.MAR_TOKEN_CACHED, n, slot0=0)
         yh2 = _host(y)
         yo, idxo, _ = orc.cached_slot(0, nxt[0], n)
         np.testing.assert_array_equal(idx[0], idxo, err_msg="conditional-only step, slot 0")
-        _close(yh2[0], yo, dims.dtype, "conditional-only step, slot 0")
+        _close(yh2[0], yo, dims.dtype, "conditional-only step, slot 0", name)
         uo = torch.empty_like(guided)
         cache.cfg_combine(B.MAR_CFG_REUSE, y, None, 4.0, guided, uo)
         torch.cuda.synchronize()

@@ -475,3 +475,201 @@ def test_oracle_cfg_state():
     g2, uh = o.cfg("reuse", c, None, 3.0)
     np.testing.assert_allclose(uh, u, atol=1e-6)
     np.testing.assert_allclose(g2, g, atol=1e-5)
+
+
+# --------------------------------------------------------------------------
+# Which rows the similarity compares (Eq. 8, Sec. 4.4)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("P", [1, 2, 3])
+def test_scores_are_cosines_of_block_p_minus_1_value_rows_through_torch(P):
+    """The cached step scores the value rows of block P-1 (Sec. 4.4: the
+    value matrix, of the last always-computed block), this step's against
+    the previous step's.  Reached here through torch: encoder layers 0..P-2,
+    then layer P-1's own norm1 and the value slice of its attention in-
+    projection; the rows are stored as fp32 (the dims' storage type), and
+    torch's cosine_similarity compares them.  Scoring block P-2's value rows
+    or block P-1's LayerNorm output instead gives other scores, which this
+    test tells apart."""
+    d = MarDims(P + 2, 32, 4, 128, 12, 2, P, "f32")
+    W, o, x, prev = _setup(d)
+    layers = [_torch_layer(w, d.d_model, d.n_heads, d.d_mlp, d.ln_eps) for w in W]
+    D = d.d_model
+
+    def rows_of(inp, block, what):
+        with torch.no_grad():
+            h = torch.from_numpy(np.asarray(inp, dtype=np.float64))
+            for lay in layers[:block]:
+                h = lay(h[None])[0]
+            a = layers[block].norm1(h)
+            if what == "ln":
+                out = a
+            else:
+                attn = layers[block].self_attn
+                out = torch.nn.functional.linear(a, attn.in_proj_weight[2 * D:], attn.in_proj_bias[2 * D:])
+            return out.to(torch.float32).to(torch.float64)   # stored as fp32
+
+    def torch_scores(block, what, b):
+        cur, ref = rows_of(x[b], block, what), rows_of(prev[b], block, what)
+        return torch.nn.functional.cosine_similarity(cur, ref, dim=-1, eps=0.0).numpy()
+
+    o.full(prev)
+    _, idx, s = o.cached(x, 4)
+    for b in range(2):
+        want = torch_scores(P - 1, "v", b)
+        np.testing.assert_allclose(s[b], want, rtol=0, atol=1e-13)
+        np.testing.assert_array_equal(idx[b], np.sort(np.argsort(want, kind="stable")[:4]))
+        # the alternatives the test must tell apart
+        assert np.abs(torch_scores(P - 1, "ln", b) - s[b]).max() > 1e-6
+        if P >= 2:
+            assert np.abs(torch_scores(P - 2, "v", b) - s[b]).max() > 1e-6
+
+
+def test_scores_without_prefix_use_block_0_value_rows_of_the_input():
+    """With no always-computed block the score pass forms block 0's value
+    rows from the step input (torch: layer 0's norm1 and value slice)."""
+    d = MarDims(2, 32, 4, 128, 12, 2, 0, "f32")
+    W, o, x, prev = _setup(d)
+    lay = _torch_layer(W[0], d.d_model, d.n_heads, d.d_mlp, d.ln_eps)
+    D = d.d_model
+
+    def v_of(inp):
+        with torch.no_grad():
+            a = lay.norm1(torch.from_numpy(np.asarray(inp, dtype=np.float64)))
+            w, bias = lay.self_attn.in_proj_weight[2 * D:], lay.self_attn.in_proj_bias[2 * D:]
+            return torch.nn.functional.linear(a, w, bias).to(torch.float32).to(torch.float64)
+
+    o.full(prev)
+    _, _, s = o.cached(x, 3)
+    for b in range(2):
+        want = torch.nn.functional.cosine_similarity(v_of(x[b]), v_of(prev[b]), dim=-1, eps=0.0).numpy()
+        np.testing.assert_allclose(s[b], want, rtol=0, atol=1e-13)
+
+
+# --------------------------------------------------------------------------
+# Storage rounding (the precision the path stores values in)
+# --------------------------------------------------------------------------
+
+def _bf16_rne_from_bits(x32):
+    """Textbook round-to-nearest-even of float32 bit patterns to bfloat16,
+    on Python integers: add 0x7FFF plus the kept part's lowest bit, drop the
+    low 16 bits."""
+    import struct
+    out = []
+    for v in np.asarray(x32, dtype=np.float32).ravel().tolist():
+        bits = struct.unpack("<I", struct.pack("<f", v))[0]
+        if (bits & 0x7F800000) == 0x7F800000 and (bits & 0x7FFFFF):
+            out.append(float("nan"))
+            continue
+        r = ((bits + 0x7FFF + ((bits >> 16) & 1)) >> 16) << 16
+        out.append(struct.unpack("<f", struct.pack("<I", r & 0xFFFFFFFF))[0])
+    return np.asarray(out, dtype=np.float64)
+
+
+def test_storage_round_bf16_matches_bit_level_rounding():
+    rng = np.random.default_rng(5)
+    x = (rng.standard_normal(4000) * np.exp(rng.uniform(-30, 30, 4000))).astype(np.float32)
+    got = storage_round(x, "bf16")
+    np.testing.assert_array_equal(got, _bf16_rne_from_bits(x))
+
+
+def test_storage_round_closed_cases():
+    """Ties go to even; fp64 values take the path's fp32 step first (it
+    computes in fp32, then stores), so a bf16 tie reached only after the
+    fp32 rounding also goes to even."""
+    e = 2.0 ** -8
+    cases_bf16 = [
+        (1.0, 1.0), (1.0 + e, 1.0),                  # tie between 1 and 1 + 2^-7 -> even (1)
+        (1.0 + 3 * e, 1.0 + 4 * e),                  # tie between 1 + 2^-7 and 1 + 2^-6 -> even
+        (1.0 + e + 2.0 ** -20, 1.0 + 2 * e),         # just above the tie -> up
+        (1.0 + e + 2.0 ** -30, 1.0),                 # below fp32 resolution: fp32 gives the tie, then even
+        (-(1.0 + 3 * e), -(1.0 + 4 * e)),
+        (3.4e38, np.inf),                            # past the midpoint above bf16's largest finite value
+        (3.3e38, round(3.3e38 / 2.0 ** 120) * 2.0 ** 120),  # bf16 spacing in [2^127, 2^128) is 2^120
+        (0.0, 0.0),
+    ]
+    for x, want in cases_bf16:
+        assert storage_round(np.array([x]), "bf16")[0] == want, x
+    assert np.isnan(storage_round(np.array([np.nan]), "bf16")[0])
+    f = 2.0 ** -24
+    cases_f32 = [
+        (1.0 + f, 1.0),                              # tie between 1 and 1 + 2^-23 -> even
+        (1.0 + 3 * f, 1.0 + 4 * f),
+        (1.0 + f + 2.0 ** -40, 1.0 + 2 * f),
+        (2.0 ** -150, 0.0),                          # half the smallest subnormal -> even (0)
+        (1.5 * 2.0 ** -149, 2.0 ** -148),
+    ]
+    for x, want in cases_f32:
+        assert storage_round(np.array([x]), "f32")[0] == want, x
+    with pytest.raises(ValueError):
+        storage_round(np.array([1.0]), "fp8")
+
+
+# --------------------------------------------------------------------------
+# The storage-rounding emulation (sizes the bf16 tolerance at full depth)
+# --------------------------------------------------------------------------
+
+def test_emulated_attention_special_cases():
+    from oracle.storage_emulation import attention_stored
+    rng = np.random.default_rng(3)
+    q, k, v = (rng.standard_normal((5, 8)) for _ in range(3))
+    # fp32 storage keeps the probabilities: the oracle's attention
+    np.testing.assert_allclose(attention_stored(q, k, v, "f32"), attention(q, k, v), rtol=0, atol=1e-14)
+    # one key: the probability is exactly 1, the output its value row
+    np.testing.assert_array_equal(attention_stored(q, k[:1], v[:1], "bf16"), np.repeat(v[:1], 5, axis=0))
+    # equal logits: every probability is exactly 1, the output the mean
+    np.testing.assert_allclose(attention_stored(np.zeros((2, 8)), k, v, "bf16"),
+                               np.repeat(v.mean(axis=0, keepdims=True), 2, axis=0), rtol=0, atol=1e-15)
+    # otherwise the bf16 weights move the result by about a bf16 step
+    d = np.abs(attention_stored(q, k, v, "bf16") - attention(q, k, v)).max()
+    assert 1e-6 < d < 2e-2
+
+
+def test_emulated_block_is_the_oracle_block_up_to_storage_rounding():
+    from oracle.storage_emulation import block_rows_stored
+    d = MarDims(1, 64, 4, 256, 16, 1, 0, "bf16")
+    W = _weights(d, std=0.05)
+    m = normal_rows((d.seq_len, d.d_model), seed=4)
+    rows = np.arange(d.seq_len)
+    want, v_want = block_rows(m, rows, W[0], d.n_heads, d.ln_eps)
+    got32, v32 = block_rows_stored(m, rows, W[0], d.n_heads, d.ln_eps, "f32")
+    got16, v16 = block_rows_stored(m, rows, W[0], d.n_heads, d.ln_eps, "bf16")
+    # fp32 storage: within fp32 resolution of the exact block
+    np.testing.assert_allclose(got32, want, rtol=1e-5, atol=1e-5)
+    # bf16 storage: a bf16-sized deviation, present but small
+    dev16 = np.abs(got16 - want).max()
+    assert 1e-4 < dev16 < 5e-2
+    # the value rows are returned as stored
+    np.testing.assert_array_equal(v16, storage_round(v16, "bf16"))
+    np.testing.assert_array_equal(v32, storage_round(v32, "f32"))
+    # subset rows equal the same rows of the whole block
+    sub = np.array([1, 5, 9])
+    got_sub, _ = block_rows_stored(m, sub, W[0], d.n_heads, d.ln_eps, "bf16")
+    np.testing.assert_array_equal(got_sub, got16[sub])
+
+
+@pytest.mark.parametrize("P", [0, 2])
+def test_emulated_step_keeps_the_method_invariants(P):
+    """The emulation runs the oracle's step: N = S reproduces its own full
+    step, unchanged input reuses exactly, cached rows are copies."""
+    from oracle.storage_emulation import StorageEmulation
+    d = MarDims(3, 32, 4, 128, 12, 2, P, "bf16")
+    W = _weights(d)
+    x = normal_rows((2, d.seq_len, d.d_model), seed=1, dtype="bf16")
+    prev = perturbed(x, seed=2, std=0.3, dtype="bf16")
+    e = StorageEmulation(d, W)
+    y_prev = e.full(prev)
+    y, idx, _ = e.cached(x, 4)
+    for b in range(2):
+        keep = np.setdiff1d(np.arange(d.seq_len), idx[b])
+        np.testing.assert_array_equal(y[b, keep], y_prev[b, keep])
+    e2 = StorageEmulation(d, W)
+    e2.full(prev)
+    y_all, idx_all, _ = e2.cached(x, d.seq_len)
+    np.testing.assert_array_equal(idx_all[0], np.arange(d.seq_len))
+    np.testing.assert_allclose(y_all, StorageEmulation(d, W).full(x), rtol=0, atol=1e-12)
+    e3 = StorageEmulation(d, W)
+    y3 = e3.full(x)
+    y4, _, s4 = e3.cached(x, 5)
+    assert np.all(s4 == 1.0)
+    np.testing.assert_array_equal(y4, y3)
