@@ -1,0 +1,191 @@
+"""Pins of the diffusion-head oracle (oracle/diffusion_head.py) against what
+the paper, the DDPM algebra and library routines fix.  CPU only; nothing here
+runs the GPU library."""
+import math
+import os
+from dataclasses import replace
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import diffusion_head as DH
+from oracle.mar_oracle import linear
+from paper_2503_12450_amd.workload import HEADS, HeadDims, head_weights, normal_rows
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "table1_mar_baseline_flops.txt")
+TINY = HeadDims(width=64, depth=3, cond_dim=48, token_dim=16, steps=10, train_steps=100, freq_dim=32)
+
+
+def _table1():
+    rows = {}
+    for line in open(GOLDEN):
+        if line.startswith("#") or not line.strip():
+            continue
+        model, steps, tf = line.split()
+        rows.setdefault(model, {})[int(steps)] = float(tf)
+    return rows
+
+
+def test_head_size_reproduces_table1_constant():
+    """Table 1's baseline FLOPs are linear in the decoding steps; the
+    constant term does not depend on them: it is the per-token head, run
+    for 256 tokens x 2 guidance pathways x 100 diffusion steps per image.
+    The head sizes reproduce it within 5 %."""
+    t1 = _table1()
+    for model, hd in HEADS.items():
+        ks = sorted(t1[model])
+        slope, const = np.polyfit(ks, [t1[model][k] for k in ks], 1)
+        head = DH.head_flops_per_eval(hd) * 256 * 2 * hd.steps / 1e12
+        assert abs(head / const - 1) < 0.05, (model, head, const)
+
+
+def test_silu_and_plain_layer_norm_match_torch():
+    x = np.random.default_rng(0).standard_normal((6, 40)) * 3
+    np.testing.assert_allclose(DH.silu(x), torch.nn.functional.silu(torch.from_numpy(x)).numpy(),
+                               rtol=0, atol=1e-14)
+    ref = torch.nn.functional.layer_norm(torch.from_numpy(x), (40,), eps=1e-6).numpy()
+    np.testing.assert_allclose(DH.plain_layer_norm(x, 1e-6), ref, rtol=0, atol=1e-13)
+    assert DH.silu(np.array([0.0]))[0] == 0.0
+
+
+def test_timestep_features_closed_form():
+    f = DH.timestep_features(np.array([0, 7]), 16)
+    np.testing.assert_array_equal(f[0], np.r_[np.ones(8), np.zeros(8)])
+    # the first frequency is 1: column 0 is cos(t), column 8 sin(t)
+    assert f[1, 0] == math.cos(7.0) and f[1, 8] == math.sin(7.0)
+    # the last frequency is 10000^(-7/8)
+    assert abs(f[1, 7] - math.cos(7.0 * 10000.0 ** (-7 / 8))) < 1e-15
+
+
+def test_schedule_closed_forms():
+    hd = replace(TINY, steps=100, train_steps=100)
+    s = DH.ddpm_schedule(hd)
+    betas = torch.linspace(1e-4, 0.02, 100, dtype=torch.float64)
+    # without respacing the betas are the training betas themselves
+    np.testing.assert_allclose(s["beta"], betas.numpy(), rtol=1e-12, atol=0)
+    np.testing.assert_allclose(s["abar"], torch.cumprod(1 - betas, 0).numpy(), rtol=1e-14, atol=0)
+    # respaced to 10 steps: timesteps 0, 10, ..., 90 and the product of the
+    # skipped alphas as each step's alpha
+    r = DH.ddpm_schedule(replace(hd, steps=10))
+    np.testing.assert_array_equal(r["t"], np.arange(0, 100, 10))
+    full = torch.cumprod(1 - betas, 0).numpy()
+    np.testing.assert_allclose(1 - r["beta"][3], full[30] / full[20], rtol=1e-12)
+    assert r["sigma"][0] == 0.0
+    i = 5
+    post = r["beta"][i] * (1 - r["abar"][i - 1]) / (1 - r["abar"][i])
+    assert abs(r["sigma"][i] ** 2 - post) < 1e-15
+
+
+@pytest.mark.parametrize("i", [0, 3, 9])
+def test_ddpm_step_with_true_noise_is_the_posterior_mean(i):
+    """x_i = sqrt(abar) x0 + sqrt(1 - abar) eps; predicting eps exactly, the
+    noise-free step lands on the posterior mean of q(x_(i-1) | x_i, x0)
+    written in its other form (Ho et al. 2020, Eq. 7); at the last step it
+    is x0 itself."""
+    s = DH.ddpm_schedule(TINY)
+    rng = np.random.default_rng(i)
+    x0, eps = rng.standard_normal((4, 16)), rng.standard_normal((4, 16))
+    ab = s["abar"][i]
+    ab_prev = s["abar"][i - 1] if i > 0 else 1.0
+    beta = s["beta"][i]
+    xt = math.sqrt(ab) * x0 + math.sqrt(1 - ab) * eps
+    got = DH.ddpm_step(xt, eps, i, s, np.zeros_like(x0))
+    mu = (math.sqrt(ab_prev) * beta / (1 - ab)) * x0 + (math.sqrt(1 - beta) * (1 - ab_prev) / (1 - ab)) * xt
+    np.testing.assert_allclose(got, mu, rtol=0, atol=1e-12)
+    if i == 0:
+        np.testing.assert_allclose(got, x0, rtol=0, atol=1e-12)
+    # the noise enters with sigma_i
+    xi = rng.standard_normal((4, 16))
+    np.testing.assert_allclose(DH.ddpm_step(xt, eps, i, s, xi) - got, s["sigma"][i] * xi, rtol=0, atol=1e-14)
+
+
+class _TorchHead(torch.nn.Module):
+    """The same network written with torch modules."""
+
+    def __init__(self, hd, W):
+        super().__init__()
+        t = lambda a: torch.from_numpy(np.asarray(a, dtype=np.float64))  # noqa: E731
+
+        def lin(wk, bk, i=None):
+            w = W[wk] if i is None else W[wk][i]
+            b = W[bk] if i is None else W[bk][i]
+            m = torch.nn.Linear(w.shape[1], w.shape[0], dtype=torch.float64)
+            with torch.no_grad():
+                m.weight.copy_(t(w))
+                m.bias.copy_(t(b))
+            return m
+
+        self.hd = hd
+        self.z, self.inp, self.ada, self.out = lin("z_w", "z_b"), lin("in_w", "in_b"), lin("ada_w", "ada_b"), \
+            lin("out_w", "out_b")
+        self.fc1 = torch.nn.ModuleList([lin("fc1_w", "fc1_b", k) for k in range(hd.depth)])
+        self.fc2 = torch.nn.ModuleList([lin("fc2_w", "fc2_b", k) for k in range(hd.depth)])
+        self.ln = torch.nn.LayerNorm(hd.width, eps=hd.ln_eps, elementwise_affine=False, dtype=torch.float64)
+
+    def forward(self, x, e, z):
+        mods = self.ada(torch.nn.functional.silu(self.z(z) + e)).chunk(self.hd.n_mod, dim=-1)
+        h = self.inp(x)
+        for k in range(self.hd.depth):
+            shift, scale, gate = mods[3 * k:3 * k + 3]
+            u = self.ln(h) * (1 + scale) + shift
+            h = h + gate * self.fc2[k](torch.nn.functional.silu(self.fc1[k](u)))
+        return self.out(self.ln(h) * (1 + mods[-1]) + mods[-2])
+
+
+def test_head_matches_torch_modules():
+    hd = replace(TINY, dtype="f32")
+    W = head_weights(hd, std=0.2)
+    x = normal_rows((7, hd.token_dim), seed=1)
+    z = normal_rows((7, hd.cond_dim), seed=2)
+    e = DH.time_embeddings(hd, W)
+    # time embedding through torch too
+    phi = torch.from_numpy(DH.timestep_features(DH.ddpm_schedule(hd)["t"], hd.freq_dim))
+    t1 = torch.nn.functional.linear(phi, torch.from_numpy(W["t1_w"].astype(np.float64)),
+                                    torch.from_numpy(W["t1_b"].astype(np.float64)))
+    e_ref = torch.nn.functional.linear(torch.nn.functional.silu(t1), torch.from_numpy(W["t2_w"].astype(np.float64)),
+                                       torch.from_numpy(W["t2_b"].astype(np.float64))).numpy()
+    np.testing.assert_allclose(e, e_ref, rtol=0, atol=1e-13)
+    ref = _TorchHead(hd, W)
+    with torch.no_grad():
+        want = ref(torch.from_numpy(x.astype(np.float64)), torch.from_numpy(e[4]),
+                   torch.from_numpy(z.astype(np.float64))).numpy()
+    np.testing.assert_allclose(DH.head_eps(x, e[4], z, W, hd), want, rtol=0, atol=1e-12)
+
+
+def test_head_with_zero_gates_skips_every_block():
+    hd = replace(TINY, dtype="f32")
+    W = head_weights(hd, std=0.2)
+    w = hd.width
+    for k in range(hd.depth):
+        rows = slice((3 * k + 2) * w, (3 * k + 3) * w)
+        W["ada_w"][rows] = 0.0
+        W["ada_b"][rows] = 0.0
+    x = normal_rows((5, hd.token_dim), seed=1)
+    z = normal_rows((5, hd.cond_dim), seed=2)
+    e = DH.time_embeddings(hd, W)[2]
+    m = linear(DH.silu(linear(z, W["z_w"], W["z_b"]) + e), W["ada_w"], W["ada_b"])
+    h = linear(x, W["in_w"], W["in_b"])
+    u = DH.plain_layer_norm(h, hd.ln_eps) * (1 + m[:, -w:]) + m[:, -2 * w:-w]
+    np.testing.assert_allclose(DH.head_eps(x, e, z, W, hd), linear(u, W["out_w"], W["out_b"]), rtol=0, atol=1e-13)
+
+
+def test_guidance_closed_forms_and_sampler_invariance():
+    rng = np.random.default_rng(4)
+    ec, eu = rng.standard_normal((3, 16)), rng.standard_normal((3, 16))
+    np.testing.assert_array_equal(DH.guided_eps(ec, eu, 0.0), eu)
+    np.testing.assert_allclose(DH.guided_eps(ec, eu, 1.0), ec, rtol=0, atol=1e-15)
+    # with identical conditional and unconditional rows the scale does not matter
+    hd = replace(TINY, dtype="f32")
+    W = head_weights(hd, std=0.2)
+    z = normal_rows((4, hd.cond_dim), seed=2)
+    x0 = normal_rows((4, hd.token_dim), seed=3)
+    xi = normal_rows((hd.steps, 4, hd.token_dim), seed=5)
+    a = DH.sample(z, z, x0, xi, 1.0, W, hd)
+    b = DH.sample(z, z, x0, xi, 7.5, W, hd)
+    np.testing.assert_array_equal(a, b)
+    # the trajectory starts at the initial noise and ends at the result
+    tr = DH.sample(z, z, x0, xi, 3.0, W, hd, trajectory=True)
+    assert tr.shape == (hd.steps + 1, 4, hd.token_dim)
+    np.testing.assert_array_equal(tr[0], x0)
+    np.testing.assert_array_equal(tr[-1], a)
