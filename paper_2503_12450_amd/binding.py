@@ -1,7 +1,7 @@
 """ctypes binding of libmarcache.so (argument marshalling only).
 
-Every function here forwards to the C ABI declared in include/mar_cache.h
-and include/mar_kernels.h; every step of the computation runs in the HIP
+Every function here forwards to the C ABI declared in include/mar_cache.h,
+include/mar_kernels.h and include/mar_head.h; every step of the computation runs in the HIP
 library.  PyTorch supplies device memory and the current stream.  There is
 no fallback: if the library is missing or fails to load, an ImportError /
 OSError is raised.
@@ -32,8 +32,9 @@ EXPORTED = (
     "mar_k_layernorm", "mar_k_linear", "mar_k_linear_residual", "mar_k_qkv",
     "mar_k_attention", "mar_k_scores", "mar_k_select", "mar_k_select_most_similar",
     "mar_k_gemm_variant",
+    "mar_head_workspace_bytes", "mar_head_init", "mar_head_sample", "mar_head_destroy",
 )
-GEMM_VARIANTS = 12
+GEMM_VARIANTS = 14
 
 
 class MarError(RuntimeError):
@@ -57,6 +58,21 @@ WEIGHT_FIELDS = ("ln1_w", "ln1_b", "qkv_w", "qkv_b", "proj_w", "proj_b",
 
 class MarBlockWeightsC(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in WEIGHT_FIELDS]
+
+
+class MarHeadDimsC(ctypes.Structure):
+    _fields_ = [("width", ctypes.c_int32), ("depth", ctypes.c_int32), ("cond_dim", ctypes.c_int32),
+                ("token_dim", ctypes.c_int32), ("steps", ctypes.c_int32), ("train_steps", ctypes.c_int32),
+                ("freq_dim", ctypes.c_int32), ("max_rows", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("beta_start", ctypes.c_float), ("beta_end", ctypes.c_float), ("ln_eps", ctypes.c_float)]
+
+
+HEAD_WEIGHT_FIELDS = ("z_w", "z_b", "t1_w", "t1_b", "t2_w", "t2_b", "in_w", "in_b", "ada_w", "ada_b",
+                      "fc1_w", "fc1_b", "fc2_w", "fc2_b", "out_w", "out_b")
+
+
+class MarHeadWeightsC(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in HEAD_WEIGHT_FIELDS]
 
 
 _vp, _i32, _f32, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
@@ -83,6 +99,11 @@ _SIGNATURES = {
     "mar_k_select": (_i32, [_vp, _i32, _i32, _i32, _vp, _vp]),
     "mar_k_select_most_similar": (_i32, [_vp, _i32, _i32, _i32, _vp, _vp]),
     "mar_k_gemm_variant": (_i32, [_i32]),
+    "mar_head_workspace_bytes": (_sz, [ctypes.POINTER(MarHeadDimsC)]),
+    "mar_head_init": (_i32, [ctypes.POINTER(MarHeadDimsC), ctypes.POINTER(MarHeadWeightsC), _vp, _sz, _vp,
+                             ctypes.POINTER(_vp)]),
+    "mar_head_sample": (_i32, [_vp, _vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _f32, _vp, _vp, _vp, _vp]),
+    "mar_head_destroy": (_i32, [_vp]),
 }
 
 _lib: Optional[ctypes.CDLL] = None
@@ -292,3 +313,62 @@ def k_select(scores, n: int, idx, stream=None, most_similar: bool = False) -> No
 def k_gemm_variant(variant: int) -> None:
     """Force a tile configuration of the matrix products (-1: by shape)."""
     _check(load().mar_k_gemm_variant(variant))
+
+
+# --------------------------------------------------------------------------
+# the diffusion head (include/mar_head.h)
+# --------------------------------------------------------------------------
+
+def head_dims_c(hd) -> MarHeadDimsC:
+    return MarHeadDimsC(hd.width, hd.depth, hd.cond_dim, hd.token_dim, hd.steps, hd.train_steps, hd.freq_dim,
+                        hd.max_rows, dtype_code(hd.dtype), hd.beta_start, hd.beta_end, hd.ln_eps)
+
+
+def head_workspace_bytes(hd) -> int:
+    d = head_dims_c(hd)
+    n = load().mar_head_workspace_bytes(ctypes.byref(d))
+    if n == 0:
+        raise MarError(MAR_E_SHAPE, load().mar_last_error().decode())
+    return n
+
+
+class MarHead:
+    """Handle over a workspace tensor; the library copies the head's weights
+    in and computes its time embeddings."""
+
+    def __init__(self, hd, weights: Dict[str, "object"], device="cuda", stream=None):
+        torch = _torch()
+        self.dims = hd
+        self.lib = load()
+        nbytes = head_workspace_bytes(hd)
+        self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+        off = (-self.workspace.data_ptr()) % 256
+        self._ws = self.workspace[off:off + nbytes]
+        w = MarHeadWeightsC(*[weights[f].data_ptr() for f in HEAD_WEIGHT_FIELDS])
+        self._weights = weights
+        handle = ctypes.c_void_p()
+        d = head_dims_c(hd)
+        _check(self.lib.mar_head_init(ctypes.byref(d), ctypes.byref(w), self._ws.data_ptr(), nbytes,
+                                      _stream(stream), ctypes.byref(handle)))
+        self.handle = handle
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            self.lib.mar_head_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def sample(self, y_cond, y_uncond, row_cond, row_uncond, x_init, xi, scale: float, x_out,
+               trajectory=None, eps_out=None, stream=None) -> None:
+        """y_cond, y_uncond: [y_rows, cond_dim] fp32 (any leading shape
+        flattened); row_*: int32 [rows]; x_init [rows, T]; xi [steps, rows, T]."""
+        y_rows = y_cond.numel() // self.dims.cond_dim
+        _check(self.lib.mar_head_sample(self.handle, y_cond.data_ptr(), y_uncond.data_ptr(), y_rows,
+                                        row_cond.data_ptr(), row_uncond.data_ptr(), row_cond.shape[0],
+                                        x_init.data_ptr(), xi.data_ptr(), float(scale), x_out.data_ptr(),
+                                        _ptr(trajectory), _ptr(eps_out), _stream(stream)))

@@ -16,18 +16,26 @@
 
 using namespace marcache;
 
-namespace {
-
 // The last error of this thread, in a fixed buffer: reporting an error never
 // allocates, so nothing can throw across the C boundary from here.
-thread_local char g_err[512];
+static thread_local char g_err[512];
 
-void clear_error() { g_err[0] = '\0'; }
+namespace marcache {
+void abi_clear_error() { g_err[0] = '\0'; }
+int abi_fail_v(int s, const char* fmt, va_list ap) {
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  return s;
+}
+}  // namespace marcache
+
+namespace {
+
+void clear_error() { abi_clear_error(); }
 
 mar_status fail(mar_status s, const char* fmt, ...) {
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  abi_fail_v(s, fmt, ap);
   va_end(ap);
   return s;
 }

@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stdarg.h>
 #include <stdint.h>
 
 namespace marcache {
@@ -109,6 +110,11 @@ __device__ __forceinline__ double wave_sum(double v) {
   return v;
 }
 
+// The thread-local message behind mar_last_error(): cleared at the start of
+// every C entry point, set by a failing one (never allocates).
+void abi_clear_error();
+int abi_fail_v(int status, const char* fmt, va_list ap);
+
 // ---------------------------------------------------------------------------
 // Launchers (host side).  All return hipSuccess or the launch error.
 // Rows of a "slot-mapped" matrix: row m belongs to slot m / per_slot and to
@@ -129,7 +135,9 @@ enum EpiKind {
   EPI_BIAS = 0,      // out[m, n] = C + bias[n]                        (dtype)
   EPI_GELU = 1,      // out[m, n] = gelu(C + bias[n])                  (dtype)
   EPI_RESIDUAL = 2,  // out[row(m), n] = resid[m, n] + C + bias[n]     (fp32)
-  EPI_QKV = 3        // split into q rows and key/value cache rows     (dtype)
+  EPI_QKV = 3,       // split into q rows and key/value cache rows     (dtype)
+  EPI_SILU = 4,      // out[m, n] = silu(C + bias[n])                  (bf16 only)
+  EPI_GATE = 5       // out[m, n] = resid[m, n] + gate[m, n] (C + bias[n])  (fp32; bf16 only)
 };
 
 struct EpiArgs {
@@ -157,6 +165,9 @@ struct EpiArgs {
   void* k_cache;
   void* v_cache;
   void* v_copy;  // nullable: value rows again, [slot][head][tok][d]
+  // GATE: gate[m, n] = gate[m * gate_ld + n] in the storage dtype
+  const void* gate;
+  int gate_ld;
 };
 
 hipError_t launch_gemm(int dtype, const void* A, const void* W, int M, int N, int K,

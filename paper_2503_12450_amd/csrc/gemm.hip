@@ -28,6 +28,9 @@
 //                                              fp32, 7.1.27 for bf16 output)
 //   RESIDUAL  out[row'] = resid + C + b       (fp32; row' may scatter into
 //                                              the output cache, Eq. 9)
+//   SILU      out = silu(C + b)               (bf16)
+//   GATE      out = resid + gate (C + b)      (fp32; the gated residual of
+//                                              the diffusion head's blocks)
 //   QKV       q rows, and keys/values written straight into the per-block
 //             cache at the row's (slot, token): the cache update of Eq. 9.
 //             Keys and values are both stored [slot, head, token, d]
@@ -94,6 +97,14 @@ __device__ __forceinline__ float gelu_erf_bf16(float x) {
   const float r = __builtin_amdgcn_rcpf(d);
   const float r2 = r * r;
   return fmaf(-(ax * r2), r2, fmaxf(x, 0.0f));
+}
+
+// silu(x) = x / (1 + e^-x), with the hardware exp2 and reciprocal (each
+// within a few fp32 ulps; the result is stored in bf16).  For x below
+// about -88 the exponential overflows to +inf and the quotient is -0,
+// the limit.
+__device__ __forceinline__ float silu_f(float x) {
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * x));
 }
 
 typedef __attribute__((ext_vector_type(4))) int i32x4_t;
@@ -206,6 +217,14 @@ __device__ __forceinline__ EpiCtx<T, KIND> make_epi(const EpiArgs& e, int M, int
   if constexpr (KIND == EPI_BIAS || KIND == EPI_GELU) {
     c.out = make_out(e.out, static_cast<unsigned>(M) * N * ES);
     c.aux0 = c.aux1 = c.aux2 = c.out;
+  } else if constexpr (KIND == EPI_SILU) {
+    c.out = make_out(e.out, static_cast<unsigned>(M) * N * ES);
+    c.aux0 = c.aux1 = c.aux2 = c.out;
+  } else if constexpr (KIND == EPI_GATE) {
+    c.out = make_out(e.out, static_cast<unsigned>(M) * N * 4u);
+    c.aux0 = make_out(const_cast<float*>(e.resid), static_cast<unsigned>(M) * N * 4u);
+    c.aux1 = c.aux0;
+    c.aux2 = make_out(const_cast<void*>(e.gate), static_cast<unsigned>(M) * e.gate_ld * ES);
   } else if constexpr (KIND == EPI_RESIDUAL) {
     const unsigned rows = e.out_idx ? static_cast<unsigned>((M + e.per_slot - 1) / e.per_slot) * e.seq
                                     : static_cast<unsigned>(M);
@@ -233,7 +252,7 @@ __device__ __forceinline__ int qkv_section(const EpiArgs& e, int ng) {
 // columns n_wave + 0..WN-1; sb is the bias of those columns (LDS), reg the
 // wave's LDS staging region (32 * WN * 4 bytes).
 template <typename T, int KIND>
-using EpiOut = typename std::conditional<KIND == EPI_RESIDUAL, float, T>::type;  // output type
+using EpiOut = typename std::conditional<KIND == EPI_RESIDUAL || KIND == EPI_GATE, float, T>::type;  // output type
 
 // Rows r0 .. r0 + HS - 1 of the strip go through LDS in one pass (HS = 32,
 // or 16 when a 32-row region per wave does not fit the staging space).
@@ -264,6 +283,7 @@ __device__ __forceinline__ void epilogue_strip(const EpiArgs& e, const EpiCtx<T,
       for (int r = 0; r < 4; ++r) {
         x[g][r] = acc[j][4 * g + r] + bv[r];
         if constexpr (KIND == EPI_GELU) x[g][r] = sizeof(T) == 2 ? gelu_erf_bf16(x[g][r]) : gelu_erf(x[g][r]);
+        if constexpr (KIND == EPI_SILU) x[g][r] = silu_f(x[g][r]);
       }
       const int colb = (32 * j + 8 * g + h4) * OS;
       if (in_pass)
@@ -289,11 +309,36 @@ __device__ __forceinline__ void epilogue_strip(const EpiArgs& e, const EpiCtx<T,
     mrow[it] = m_strip + r0 + r;
     ncol[it] = n_wave + ch * COLS;
   }
-  if constexpr (KIND == EPI_BIAS || KIND == EPI_GELU) {
+  if constexpr (KIND == EPI_BIAS || KIND == EPI_GELU || KIND == EPI_SILU) {
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const bool ok = mrow[it] < M && ncol[it] < N;
       bstore16(c.out, ok ? (mrow[it] * N + ncol[it]) * OS : kOob, val[it]);
+    }
+  } else if constexpr (KIND == EPI_GATE) {
+    // y = resid + gate (C + b): four fp32 residual values and four gates
+    // (8 bytes of bf16) per chunk, all loaded before the first store
+    u32x4_t res[IT];
+    u32x2_t gt[IT];
+    int lin[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const bool ok = mrow[it] < M && ncol[it] < N;
+      const int mc = min(mrow[it], M - 1);
+      lin[it] = ok ? (mc * N + ncol[it]) * 4 : kOob;
+      res[it] = bload16(c.aux0, lin[it]);
+      gt[it] = __builtin_amdgcn_raw_buffer_load_b64(c.aux2, ok ? (mc * e.gate_ld + ncol[it]) * 2 : kOob, 0, 0);
+    }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      u32x4_t y;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t gw = gt[it][q >> 1];
+        const float g = __uint_as_float((q & 1) ? (gw & 0xFFFF0000u) : (gw << 16));
+        y[q] = __float_as_uint(fmaf(g, __uint_as_float(val[it][q]), __uint_as_float(res[it][q])));
+      }
+      bstore16(c.out, lin[it], y);
     }
   } else if constexpr (KIND == EPI_RESIDUAL) {
     u32x4_t res[IT];
@@ -412,7 +457,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(const T* _
   // which only makes the waits that count on this number stricter.
   constexpr int EPI_IT = HS * (EC * OSZ / 16) / 64;
   constexpr int EPI_STRIPS = TM * (TN / (EC / 32)) * (32 / HS);
-  constexpr int EPI_OPS = EPI_STRIPS * EPI_IT * (KIND == EPI_RESIDUAL ? 2 : KIND == EPI_QKV ? 3 : 1);
+  constexpr int EPI_OPS = EPI_STRIPS * EPI_IT * (KIND == EPI_RESIDUAL ? 2 : (KIND == EPI_QKV || KIND == EPI_GATE) ? 3 : 1);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -727,6 +772,8 @@ int g_gemm_variant = -1;  // test hook: force a variant (-1 = by shape)
 template <typename T, int KIND>
 static hipError_t gemm_pick(const void* A, const void* W, int M, int N, int K, const EpiArgs& e,
                             hipStream_t st) {
+  constexpr bool kResid = KIND == EPI_RESIDUAL || KIND == EPI_GATE;
+  constexpr bool kAct = KIND == EPI_GELU || KIND == EPI_SILU;
   int v = g_gemm_variant;
   if (v < 0) {
     // measured on MI355X over the MAR-L schedule's shapes (d_model 1024, M
@@ -735,33 +782,38 @@ static hipError_t gemm_pick(const void* A, const void* W, int M, int N, int K, c
     // CU (early free) for the fp32 residual products and the bias products
     // in the middle range, where they balance better; otherwise 256 x 256
     // tiles with a two-stage ring of 128-byte slices, launched persistent
-    // once there are several tiles per CU
+    // once there are several tiles per CU.  Products too small to give
+    // even 128 tiles of 128 x 128 (the diffusion head's, a few hundred
+    // rows) take 64 x 64 tiles, four times as many workgroups.
     const long big = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
     const long small = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
-    if (small <= 256)
+    if (small < 128)
+      v = 6;
+    else if (small <= 256)
       v = 1;
-    else if (KIND == EPI_RESIDUAL)
-      v = big <= 512 ? 4 : 6;
+    else if (kResid)
+      v = big <= 512 ? 4 : 7;
     else if (big <= 512)
-      v = KIND == EPI_GELU || big <= 256 ? 0 : 4;
+      v = kAct || big <= 256 ? 0 : 4;
     else
-      v = big <= 1280 ? 0 : 6;
+      v = big <= 1280 ? 0 : 7;
   }
-  // variants 6..11: the configurations of 0..5 launched persistent
-  const bool persist = v >= 6;
-  if (persist) v -= 6;
+  // variants 7..13: the configurations of 0..6 launched persistent
+  const bool persist = v >= 7;
+  if (persist) v -= 7;
   // a ring needs a minimum number of slices per tile (two for the two-stage
   // rings, which load two slices ahead; S-1 for S stages): short K takes
   // 128 x 128 tiles with 64-byte slices (K * sizeof(T) is a multiple of 128)
-  static const int kMinSlices[6] = {2, 2, 2, 2, 2, 3}, kRowB[6] = {128, 128, 128, 128, 128, 64};
-  if (K * static_cast<int>(sizeof(T)) / kRowB[v] < kMinSlices[v]) v = 6;
+  static const int kMinSlices[7] = {2, 2, 2, 2, 2, 3, 2}, kRowB[7] = {128, 128, 128, 128, 128, 64, 128};
+  if (K * static_cast<int>(sizeof(T)) / kRowB[v] < kMinSlices[v]) v = 7;
   switch (v) {
-    case 6: return gemm_launch<T, 128, 128, 2, 2, 2, 64, KIND>(A, W, M, N, K, e, persist, st);
+    case 7: return gemm_launch<T, 128, 128, 2, 2, 2, 64, KIND>(A, W, M, N, K, e, persist, st);
     case 0: return gemm_launch<T, 256, 256, 2, 4, 2, 128, KIND>(A, W, M, N, K, e, persist, st);
     case 1: return gemm_launch<T, 128, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);
     case 2: return gemm_launch<T, 256, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);
     case 3: return gemm_launch<T, 128, 256, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);
     case 5: return gemm_launch<T, 256, 256, 2, 4, 4, 64, KIND>(A, W, M, N, K, e, persist, st);
+    case 6: return gemm_launch<T, 64, 64, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);
     default: return gemm_launch<T, 128, 128, 2, 2, 2, 128, KIND>(A, W, M, N, K, e, persist, st);
   }
 }
@@ -774,8 +826,17 @@ static hipError_t gemm_kind(const void* A, const void* W, int M, int N, int K, c
     case EPI_GELU: return gemm_pick<T, EPI_GELU>(A, W, M, N, K, e, st);
     case EPI_RESIDUAL: return gemm_pick<T, EPI_RESIDUAL>(A, W, M, N, K, e, st);
     case EPI_QKV: return gemm_pick<T, EPI_QKV>(A, W, M, N, K, e, st);
-    default: return hipErrorInvalidValue;
+    default: break;
   }
+  // the diffusion head's epilogues exist for bf16 operands only
+  if constexpr (std::is_same<T, bf16_t>::value) {
+    switch (e.kind) {
+      case EPI_SILU: return gemm_pick<T, EPI_SILU>(A, W, M, N, K, e, st);
+      case EPI_GATE: return gemm_pick<T, EPI_GATE>(A, W, M, N, K, e, st);
+      default: break;
+    }
+  }
+  return hipErrorInvalidValue;
 }
 
 void set_gemm_variant(int v) { g_gemm_variant = v; }
@@ -808,6 +869,8 @@ hipError_t launch_gemm(int dtype, const void* A, const void* W, int M, int N, in
     return hipErrorInvalidValue;
   if (e.kind == EPI_QKV && static_cast<size_t>((M + e.per_slot - 1) / e.per_slot) * e.n_heads * e.seq *
                                    e.d_head * es >= lim)
+    return hipErrorInvalidValue;
+  if (e.kind == EPI_GATE && (e.gate_ld < N || e.gate_ld % 4 || static_cast<size_t>(M) * e.gate_ld * es >= lim))
     return hipErrorInvalidValue;
   if (dtype == DT_BF16) return gemm_kind<bf16_t>(A, W, M, N, K, e, st);
   return gemm_kind<float>(A, W, M, N, K, e, st);

@@ -7,6 +7,8 @@ import numpy as np
 
 from .workload import MATRIX_NAMES
 
+HEAD_MATRIX_NAMES = ("z_w", "t1_w", "t2_w", "in_w", "ada_w", "fc1_w", "fc2_w", "out_w")
+
 
 def torch_dtype(dtype: str):
     import torch
@@ -26,3 +28,8 @@ def upload_blocks(blocks: Sequence[Dict[str, np.ndarray]], dtype: str, device="c
     for blk in blocks:
         out.append({k: to_device(v, dtype if k in MATRIX_NAMES else "f32", device) for k, v in blk.items()})
     return out
+
+
+def upload_head(weights: Dict[str, np.ndarray], dtype: str, device="cuda") -> Dict[str, object]:
+    """The diffusion head's matrices in the storage dtype, biases fp32."""
+    return {k: to_device(v, dtype if k in HEAD_MATRIX_NAMES else "f32", device) for k, v in weights.items()}

@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include "mar_cache.h"
+#include "mar_head.h"
 #include "mar_kernels.h"
 
 static int failures = 0;
@@ -77,8 +78,40 @@ int main(void) {
   CHECK(mar_k_select_most_similar(NULL, 1, 8, 2, NULL, NULL) == MAR_E_ARG);
   CHECK(mar_cache_destroy(NULL) == MAR_OK);
   CHECK(mar_output(NULL) == NULL);
-  CHECK(mar_k_gemm_variant(12) == MAR_E_ARG);
+  CHECK(mar_k_gemm_variant(14) == MAR_E_ARG);
   CHECK(mar_k_gemm_variant(-1) == MAR_OK);
+
+  /* the diffusion head: sizing and host-side checks */
+  {
+    mar_head_dims hd;
+    mar_head* hh = (mar_head*)&hd;
+    memset(&hd, 0, sizeof hd);
+    hd.width = 1280;
+    hd.depth = 8;
+    hd.cond_dim = 1024;
+    hd.token_dim = 16;
+    hd.steps = 100;
+    hd.train_steps = 1000;
+    hd.freq_dim = 256;
+    hd.max_rows = 1024;
+    hd.dtype = MAR_BF16;
+    hd.beta_start = 1e-4f;
+    hd.beta_end = 0.02f;
+    hd.ln_eps = 1e-6f;
+    CHECK(mar_head_workspace_bytes(&hd) > 0);
+    hd.dtype = MAR_F32;
+    CHECK(mar_head_workspace_bytes(&hd) == 0);
+    CHECK(strstr(mar_last_error(), "bf16") != NULL);
+    hd.dtype = MAR_BF16;
+    hd.max_rows = 16384; /* the modulation rows would pass 32-bit offsets */
+    CHECK(mar_head_workspace_bytes(&hd) == 0);
+    hd.max_rows = 1024;
+    CHECK(mar_head_init(&hd, NULL, NULL, 0, NULL, &hh) == MAR_E_ARG);
+    CHECK(hh == NULL);
+    CHECK(mar_head_sample(NULL, NULL, NULL, 1, NULL, NULL, 1, NULL, NULL, 1.0f, NULL, NULL, NULL, NULL) ==
+          MAR_E_ARG);
+    CHECK(mar_head_destroy(NULL) == MAR_OK);
+  }
 
   printf("abi check: %s (%d failures)\n", failures ? "FAILED" : "ok", failures);
   return failures != 0;

@@ -15,7 +15,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def _declared():
     names = set()
-    for h in ("mar_cache.h", "mar_kernels.h"):
+    for h in ("mar_cache.h", "mar_kernels.h", "mar_head.h"):
         text = open(os.path.join(ROOT, "include", h)).read()
         text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
         names |= set(re.findall(r"\b(mar_[a-z_]+)\s*\(", text))
@@ -131,3 +131,28 @@ def test_headers_are_plain_c_and_host_entry_points_answer(tmp_path):
     run = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     assert run.returncode == 0, run.stdout + run.stderr
     assert "abi check: ok" in run.stdout
+
+
+def test_head_sizing_and_checks():
+    """The diffusion head's sizing refuses unsupported shapes and checks its
+    arguments on the host before any device call."""
+    from dataclasses import replace
+    from paper_2503_12450_amd.workload import HEADS
+    lib = B.load()
+    hd = replace(HEADS["mar-l"], max_rows=1024)
+    n = B.head_workspace_bytes(hd)
+    w, nm = hd.width, hd.n_mod
+    assert n > 2 * hd.max_rows * nm * w * 2 + nm * w * w * 2
+    assert n % 256 == 0
+    for bad in (dict(width=100), dict(depth=0), dict(token_dim=0), dict(token_dim=65), dict(steps=0),
+                dict(train_steps=50), dict(freq_dim=100), dict(dtype="f32"), dict(beta_end=1.0),
+                dict(max_rows=0), dict(max_rows=16384)):
+        with pytest.raises(B.MarError):
+            B.head_workspace_bytes(replace(hd, **bad))
+    d = B.head_dims_c(hd)
+    h = ctypes.c_void_p(1)
+    assert lib.mar_head_init(ctypes.byref(d), None, None, 0, None, ctypes.byref(h)) == B.MAR_E_ARG
+    assert h.value is None
+    assert lib.mar_head_sample(None, None, None, 1, None, None, 1, None, None, 1.0, None, None, None,
+                               None) == B.MAR_E_ARG
+    assert lib.mar_head_destroy(None) == B.MAR_OK
