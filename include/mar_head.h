@@ -122,6 +122,27 @@ mar_status mar_head_sample(mar_head* head, const float* y_cond, const float* y_u
                            const float* x_init, const float* xi, float scale, float* x_out,
                            float* trajectory, float* eps_out, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): as
+ * mar_head_sample, with the same kernels and bit-identical results, but the
+ * call's scratch (the activations of its 2 rows per token and the latents)
+ * lives in a static array of 64 MiB per GPU instead of the handle's
+ * workspace, and neither this call nor anything it calls allocates.  The
+ * array's device address is resolved once per device by mar_head_init (or
+ * by the first call on a device).
+ * Limit: the scratch of `rows` tokens, 2 (2 cond_dim + width (14 +
+ * 2 (3 depth + 2))) + 4 token_dim bytes per token plus under 2 KiB of
+ * alignment, must fit 64 MiB (MAR_E_SHAPE otherwise): 387 tokens for the
+ * MAR-L head (width 1280, 8 blocks, cond_dim 1024); `rows` is not bounded
+ * by the handle's max_rows.
+ * Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ * (two streams, two threads) race and give undefined results.  Each call
+ * clears or overwrites all of the scratch it reads. */
+mar_status mar_head_sample_noalloc(mar_head* head, const float* y_cond, const float* y_uncond, int32_t y_rows,
+                                   const int32_t* row_cond, const int32_t* row_uncond, int32_t rows,
+                                   const float* x_init, const float* xi, float scale, float* x_out,
+                                   float* trajectory, float* eps_out, void* stream);
+
 /* Release the handle (host memory only).  Accepts NULL. */
 mar_status mar_head_destroy(mar_head* head);
 

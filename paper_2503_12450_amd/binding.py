@@ -33,6 +33,7 @@ EXPORTED = (
     "mar_k_attention", "mar_k_scores", "mar_k_select", "mar_k_select_most_similar",
     "mar_k_gemm_variant",
     "mar_head_workspace_bytes", "mar_head_init", "mar_head_sample", "mar_head_destroy",
+    "mar_head_sample_noalloc",
 )
 GEMM_VARIANTS = 14
 
@@ -104,6 +105,8 @@ _SIGNATURES = {
                              ctypes.POINTER(_vp)]),
     "mar_head_sample": (_i32, [_vp, _vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _f32, _vp, _vp, _vp, _vp]),
     "mar_head_destroy": (_i32, [_vp]),
+    "mar_head_sample_noalloc": (_i32, [_vp, _vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _f32, _vp, _vp, _vp,
+                                       _vp]),
 }
 
 _lib: Optional[ctypes.CDLL] = None
@@ -364,11 +367,13 @@ class MarHead:
             pass
 
     def sample(self, y_cond, y_uncond, row_cond, row_uncond, x_init, xi, scale: float, x_out,
-               trajectory=None, eps_out=None, stream=None) -> None:
+               trajectory=None, eps_out=None, stream=None, noalloc: bool = False) -> None:
         """y_cond, y_uncond: [y_rows, cond_dim] fp32 (any leading shape
-        flattened); row_*: int32 [rows]; x_init [rows, T]; xi [steps, rows, T]."""
+        flattened); row_*: int32 [rows]; x_init [rows, T]; xi [steps, rows, T].
+        noalloc: the entry point whose scratch is the library's static array."""
         y_rows = y_cond.numel() // self.dims.cond_dim
-        _check(self.lib.mar_head_sample(self.handle, y_cond.data_ptr(), y_uncond.data_ptr(), y_rows,
+        fn = self.lib.mar_head_sample_noalloc if noalloc else self.lib.mar_head_sample
+        _check(fn(self.handle, y_cond.data_ptr(), y_uncond.data_ptr(), y_rows,
                                         row_cond.data_ptr(), row_uncond.data_ptr(), row_cond.shape[0],
                                         x_init.data_ptr(), xi.data_ptr(), float(scale), x_out.data_ptr(),
                                         _ptr(trajectory), _ptr(eps_out), _stream(stream)))

@@ -23,7 +23,9 @@
 #include <cmath>
 #include <cstdarg>
 #include <memory>
+#include <mutex>
 #include <new>
+#include <system_error>
 
 #include "../../include/mar_head.h"
 #include "common.h"
@@ -292,6 +294,19 @@ __global__ __launch_bounds__(256) void head_out_kernel(const float* __restrict__
 // Handle and C ABI
 // ---------------------------------------------------------------------------
 
+// Scratch of one call: 2R rows of the network's activations (R tokens) and
+// the R latents.
+struct HeadScratch {
+  bf16_t* a0;  // [2R, cond_dim]
+  float* c;    // [2R, w]
+  bf16_t* s;   // [2R, w]
+  bf16_t* m;   // [2R, n_mod w]
+  float* h;    // [2R, w]
+  bf16_t* u;   // [2R, w]
+  bf16_t* g;   // [2R, w]
+  float* x;    // [R, T]
+};
+
 struct mar_head {
   mar_head_dims d;
   int n_mod;
@@ -302,15 +317,7 @@ struct mar_head {
   f32x4_t* coef;   // [steps] DDPM coefficients
   bf16_t* phi;     // [steps, freq] (init only)
   bf16_t* t1o;     // [steps, w] (init only)
-  // scratch of a call (2 max_rows rows)
-  bf16_t* a0;  // [2R, cond_dim]
-  float* c;    // [2R, w]
-  bf16_t* s;   // [2R, w]
-  bf16_t* m;   // [2R, n_mod w]
-  float* h;    // [2R, w]
-  bf16_t* u;   // [2R, w]
-  bf16_t* g;   // [2R, w]
-  float* x;    // [R, T]
+  HeadScratch sc;  // in the workspace, for up to max_rows tokens
 };
 
 namespace {
@@ -338,25 +345,56 @@ mar_status check_head_dims(const mar_head_dims* d) {
   return MAR_OK;
 }
 
-// Byte offsets of every buffer in the workspace, in the order of mar_head's
-// fields; returns the total.
-size_t head_layout(const mar_head_dims& d, size_t* off) {
-  const size_t w = d.width, D = d.cond_dim, T = d.token_dim, F = d.freq_dim, S = d.steps;
-  const size_t nm = 3 * static_cast<size_t>(d.depth) + 2, L = d.depth, R2 = 2 * static_cast<size_t>(d.max_rows);
-  const size_t sizes[] = {
-      w * D * 2, w * F * 2, w * w * 2, w * T * 2, nm * w * w * 2, L * w * w * 2, L * w * w * 2, T * w * 2,
-      w * 4, w * 4, w * 4, w * 4, nm * w * 4, L * w * 4, L * w * 4, T * 4,
-      S * w * 4, S * 16, S * F * 2, S * w * 2,
-      R2 * D * 2, R2 * w * 4, R2 * w * 2, R2 * nm * w * 2, R2 * w * 4, R2 * w * 2, R2 * w * 2,
-      static_cast<size_t>(d.max_rows) * T * 4};
+// Byte offsets of the scratch of a call on `rows` tokens (256-byte
+// aligned, from 0, in the order of HeadScratch's fields); returns its size.
+constexpr int kScratchBuffers = 8;
+size_t scratch_layout(const mar_head_dims& d, size_t rows, size_t* off) {
+  const size_t w = d.width, D = d.cond_dim, T = d.token_dim;
+  const size_t nm = 3 * static_cast<size_t>(d.depth) + 2, R2 = 2 * rows;
+  const size_t sizes[kScratchBuffers] = {R2 * D * 2, R2 * w * 4, R2 * w * 2, R2 * nm * w * 2,
+                                         R2 * w * 4, R2 * w * 2, R2 * w * 2, rows * T * 4};
   size_t o = 0;
-  for (size_t k = 0; k < sizeof(sizes) / sizeof(sizes[0]); ++k) {
+  for (int k = 0; k < kScratchBuffers; ++k) {
     off[k] = o;
     o = align_up(o + sizes[k]);
   }
   return o;
 }
-constexpr int kHeadBuffers = 28;
+
+HeadScratch scratch_at(unsigned char* base, const size_t* off) {
+  HeadScratch sc;
+  sc.a0 = reinterpret_cast<bf16_t*>(base + off[0]);
+  sc.c = reinterpret_cast<float*>(base + off[1]);
+  sc.s = reinterpret_cast<bf16_t*>(base + off[2]);
+  sc.m = reinterpret_cast<bf16_t*>(base + off[3]);
+  sc.h = reinterpret_cast<float*>(base + off[4]);
+  sc.u = reinterpret_cast<bf16_t*>(base + off[5]);
+  sc.g = reinterpret_cast<bf16_t*>(base + off[6]);
+  sc.x = reinterpret_cast<float*>(base + off[7]);
+  return sc;
+}
+
+// Byte offsets of the weights and tables in the workspace (in the order of
+// mar_head's fields), followed by the scratch for max_rows tokens at
+// off[kTables]; returns the total.
+constexpr int kTables = 20;
+size_t head_layout(const mar_head_dims& d, size_t* off) {
+  const size_t w = d.width, D = d.cond_dim, T = d.token_dim, F = d.freq_dim, S = d.steps;
+  const size_t nm = 3 * static_cast<size_t>(d.depth) + 2, L = d.depth;
+  const size_t sizes[kTables] = {
+      w * D * 2, w * F * 2, w * w * 2, w * T * 2, nm * w * w * 2, L * w * w * 2, L * w * w * 2, T * w * 2,
+      w * 4, w * 4, w * 4, w * 4, nm * w * 4, L * w * 4, L * w * 4, T * 4,
+      S * w * 4, S * 16, S * F * 2, S * w * 2};
+  size_t o = 0;
+  for (int k = 0; k < kTables; ++k) {
+    off[k] = o;
+    o = align_up(o + sizes[k]);
+  }
+  off[kTables] = o;
+  size_t soff[kScratchBuffers];
+  return o + scratch_layout(d, static_cast<size_t>(d.max_rows), soff);
+}
+constexpr int kHeadBuffers = kTables + 1;
 
 template <class Kern, class... Args>
 hipError_t launch_rows(Kern k, int rows, hipStream_t st, Args... args) {
@@ -367,35 +405,37 @@ hipError_t launch_rows(Kern k, int rows, hipStream_t st, Args... args) {
 
 // ln-modulation and output kernels by the groups of 4 a lane holds
 template <int G>
-hipError_t lnmod_as(const mar_head* hd, int row0_mod_off_shift, int off_scale, int rows, hipStream_t st) {
-  return launch_rows(head_lnmod_kernel<G>, rows, st, static_cast<const float*>(hd->h),
-                     static_cast<const bf16_t*>(hd->m), hd->n_mod * hd->d.width, row0_mod_off_shift, off_scale, rows,
-                     hd->d.width, hd->d.ln_eps, hd->u);
+hipError_t lnmod_as(const mar_head* hd, const HeadScratch& sc, int off_shift, int off_scale, int rows,
+                    hipStream_t st) {
+  return launch_rows(head_lnmod_kernel<G>, rows, st, static_cast<const float*>(sc.h),
+                     static_cast<const bf16_t*>(sc.m), hd->n_mod * hd->d.width, off_shift, off_scale, rows,
+                     hd->d.width, hd->d.ln_eps, sc.u);
 }
-hipError_t launch_lnmod(const mar_head* hd, int off_shift, int off_scale, int rows, hipStream_t st) {
+hipError_t launch_lnmod(const mar_head* hd, const HeadScratch& sc, int off_shift, int off_scale, int rows,
+                        hipStream_t st) {
   const int G = (hd->d.width + 255) / 256;
-  if (G <= 2) return lnmod_as<2>(hd, off_shift, off_scale, rows, st);
-  if (G <= 4) return lnmod_as<4>(hd, off_shift, off_scale, rows, st);
-  if (G <= 8) return lnmod_as<8>(hd, off_shift, off_scale, rows, st);
-  return lnmod_as<16>(hd, off_shift, off_scale, rows, st);
+  if (G <= 2) return lnmod_as<2>(hd, sc, off_shift, off_scale, rows, st);
+  if (G <= 4) return lnmod_as<4>(hd, sc, off_shift, off_scale, rows, st);
+  if (G <= 8) return lnmod_as<8>(hd, sc, off_shift, off_scale, rows, st);
+  return lnmod_as<16>(hd, sc, off_shift, off_scale, rows, st);
 }
 template <int G>
-hipError_t out_as(const mar_head* hd, int i, const float* xi, int R, float scale, float* traj, float* eps_out,
-                  hipStream_t st) {
+hipError_t out_as(const mar_head* hd, const HeadScratch& sc, int i, const float* xi, int R, float scale,
+                  float* traj, float* eps_out, hipStream_t st) {
   const int w = hd->d.width;
-  return launch_rows(head_out_kernel<G>, R, st, static_cast<const float*>(hd->h), static_cast<const bf16_t*>(hd->m),
+  return launch_rows(head_out_kernel<G>, R, st, static_cast<const float*>(sc.h), static_cast<const bf16_t*>(sc.m),
                      hd->n_mod * w, 3 * hd->d.depth * w, (3 * hd->d.depth + 1) * w,
                      static_cast<const bf16_t*>(hd->out_w), static_cast<const float*>(hd->out_b),
-                     static_cast<const f32x4_t*>(hd->coef), i, xi, R, w, hd->d.token_dim, hd->d.ln_eps, scale, hd->x,
+                     static_cast<const f32x4_t*>(hd->coef), i, xi, R, w, hd->d.token_dim, hd->d.ln_eps, scale, sc.x,
                      traj, eps_out);
 }
-hipError_t launch_out(const mar_head* hd, int i, const float* xi, int R, float scale, float* traj, float* eps_out,
-                      hipStream_t st) {
+hipError_t launch_out(const mar_head* hd, const HeadScratch& sc, int i, const float* xi, int R, float scale,
+                      float* traj, float* eps_out, hipStream_t st) {
   const int G = (hd->d.width + 255) / 256;
-  if (G <= 2) return out_as<2>(hd, i, xi, R, scale, traj, eps_out, st);
-  if (G <= 4) return out_as<4>(hd, i, xi, R, scale, traj, eps_out, st);
-  if (G <= 8) return out_as<8>(hd, i, xi, R, scale, traj, eps_out, st);
-  return out_as<16>(hd, i, xi, R, scale, traj, eps_out, st);
+  if (G <= 2) return out_as<2>(hd, sc, i, xi, R, scale, traj, eps_out, st);
+  if (G <= 4) return out_as<4>(hd, sc, i, xi, R, scale, traj, eps_out, st);
+  if (G <= 8) return out_as<8>(hd, sc, i, xi, R, scale, traj, eps_out, st);
+  return out_as<16>(hd, sc, i, xi, R, scale, traj, eps_out, st);
 }
 
 hipError_t fill_zero(float* p, long n, hipStream_t st) {
@@ -439,14 +479,9 @@ mar_status head_init(const mar_head_dims* dims, const mar_head_weights* W, void*
   hd->coef = reinterpret_cast<f32x4_t*>(ws + off[17]);
   hd->phi = reinterpret_cast<bf16_t*>(ws + off[18]);
   hd->t1o = reinterpret_cast<bf16_t*>(ws + off[19]);
-  hd->a0 = reinterpret_cast<bf16_t*>(ws + off[20]);
-  hd->c = reinterpret_cast<float*>(ws + off[21]);
-  hd->s = reinterpret_cast<bf16_t*>(ws + off[22]);
-  hd->m = reinterpret_cast<bf16_t*>(ws + off[23]);
-  hd->h = reinterpret_cast<float*>(ws + off[24]);
-  hd->u = reinterpret_cast<bf16_t*>(ws + off[25]);
-  hd->g = reinterpret_cast<bf16_t*>(ws + off[26]);
-  hd->x = reinterpret_cast<float*>(ws + off[27]);
+  size_t soff[kScratchBuffers];
+  scratch_layout(d, static_cast<size_t>(d.max_rows), soff);
+  hd->sc = scratch_at(ws + off[kTables], soff);
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   const size_t w = d.width, D = d.cond_dim, T = d.token_dim, F = d.freq_dim, L = d.depth, nm = hd->n_mod;
@@ -481,12 +516,13 @@ mar_status head_init(const mar_head_dims* dims, const mar_head_weights* W, void*
   return MAR_OK;
 }
 
-mar_status head_sample(mar_head* hd, const float* yc, const float* yu, int32_t y_rows, const int32_t* rc,
-                       const int32_t* ru, int32_t R, const float* x_init, const float* xi, float scale,
-                       float* x_out, float* traj, float* eps_out, void* stream) {
+// Arguments of a call, checked on the host (rows against the caller's
+// limit, which the scratch behind the call must hold).
+mar_status check_sample(const mar_head* hd, const float* yc, const float* yu, int32_t y_rows, const int32_t* rc,
+                        const int32_t* ru, int32_t R, int32_t max_R, const float* x_init, const float* xi,
+                        float scale, float* x_out, float* traj, float* eps_out) {
   if (!hd) return hfail(MAR_E_ARG, "head is NULL");
-  const mar_head_dims& d = hd->d;
-  if (R < 0 || R > d.max_rows) return hfail(MAR_E_ARG, "rows %d outside [0, %d]", R, d.max_rows);
+  if (R < 0 || R > max_R) return hfail(MAR_E_ARG, "rows %d outside [0, %d]", R, max_R);
   if (R == 0) return MAR_OK;
   if (!yc || !yu || !rc || !ru || !x_init || !xi || !x_out) return hfail(MAR_E_ARG, "NULL pointer");
   if (y_rows < 1) return hfail(MAR_E_ARG, "y_rows must be >= 1");
@@ -498,56 +534,94 @@ mar_status head_sample(mar_head* hd, const float* yc, const float* yu, int32_t y
     hipError_t e = hipPeekAtLastError();
     if (e != hipSuccess) return hfail(MAR_E_DEVICE, "earlier device error: %s", hipGetErrorString(e));
   }
+  return MAR_OK;
+}
+
+// The sampler over R >= 1 tokens with the scratch `sc` (checked arguments).
+mar_status head_sample(const mar_head* hd, const HeadScratch& sc, const float* yc, const float* yu, int32_t y_rows,
+                       const int32_t* rc, const int32_t* ru, int32_t R, const float* x_init, const float* xi,
+                       float scale, float* x_out, float* traj, float* eps_out, void* stream) {
+  const mar_head_dims& d = hd->d;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int w = d.width, D = d.cond_dim, T = d.token_dim, R2 = 2 * R, nm = hd->n_mod;
   const size_t xbytes = static_cast<size_t>(R) * T * sizeof(float);
   HEAD_HIP(launch_rows(head_gather_kernel, R2, st, yc, yu, static_cast<int>(y_rows), rc, ru, static_cast<int>(R), D,
-                       hd->a0),
+                       sc.a0),
            "gather");
-  HEAD_HIP(fill_zero(hd->c, static_cast<long>(R2) * w, st), "zero fill");
+  HEAD_HIP(fill_zero(sc.c, static_cast<long>(R2) * w, st), "zero fill");
   EpiArgs ec{};
   ec.kind = EPI_RESIDUAL;
   ec.bias = hd->z_b;
-  ec.out = hd->c;
-  ec.resid = hd->c;
-  HEAD_HIP(gemm(hd->a0, hd->z_w, R2, w, D, ec, st), "conditioning product");
-  HEAD_HIP(hipMemcpyAsync(hd->x, x_init, xbytes, hipMemcpyDeviceToDevice, st), "latent copy");
+  ec.out = sc.c;
+  ec.resid = sc.c;
+  HEAD_HIP(gemm(sc.a0, hd->z_w, R2, w, D, ec, st), "conditioning product");
+  HEAD_HIP(hipMemcpyAsync(sc.x, x_init, xbytes, hipMemcpyDeviceToDevice, st), "latent copy");
   if (traj) HEAD_HIP(hipMemcpyAsync(traj, x_init, xbytes, hipMemcpyDeviceToDevice, st), "trajectory copy");
   for (int j = 0; j < d.steps; ++j) {
     const int i = d.steps - 1 - j;
-    HEAD_HIP(launch_rows(head_prologue_kernel, R2, st, static_cast<const float*>(hd->c),
-                         static_cast<const float*>(hd->e + static_cast<long>(i) * w), static_cast<const float*>(hd->x),
+    HEAD_HIP(launch_rows(head_prologue_kernel, R2, st, static_cast<const float*>(sc.c),
+                         static_cast<const float*>(hd->e + static_cast<long>(i) * w), static_cast<const float*>(sc.x),
                          static_cast<const bf16_t*>(hd->in_w), static_cast<const float*>(hd->in_b), static_cast<int>(R),
-                         w, T, hd->s, hd->h),
+                         w, T, sc.s, sc.h),
              "prologue");
     EpiArgs em{};
     em.kind = EPI_BIAS;
     em.bias = hd->ada_b;
-    em.out = hd->m;
-    HEAD_HIP(gemm(hd->s, hd->ada_w, R2, nm * w, w, em, st), "modulation product");
+    em.out = sc.m;
+    HEAD_HIP(gemm(sc.s, hd->ada_w, R2, nm * w, w, em, st), "modulation product");
     for (int k = 0; k < d.depth; ++k) {
-      HEAD_HIP(launch_lnmod(hd, 3 * k * w, (3 * k + 1) * w, R2, st), "ln-modulation");
+      HEAD_HIP(launch_lnmod(hd, sc, 3 * k * w, (3 * k + 1) * w, R2, st), "ln-modulation");
       EpiArgs e1{};
       e1.kind = EPI_SILU;
       e1.bias = hd->fc1_b + static_cast<long>(k) * w;
-      e1.out = hd->g;
-      HEAD_HIP(gemm(hd->u, static_cast<const bf16_t*>(hd->fc1_w) + static_cast<long>(k) * w * w, R2, w, w, e1, st),
+      e1.out = sc.g;
+      HEAD_HIP(gemm(sc.u, static_cast<const bf16_t*>(hd->fc1_w) + static_cast<long>(k) * w * w, R2, w, w, e1, st),
                "block first product");
       EpiArgs e2{};
       e2.kind = EPI_GATE;
       e2.bias = hd->fc2_b + static_cast<long>(k) * w;
-      e2.out = hd->h;
-      e2.resid = hd->h;
-      e2.gate = hd->m + static_cast<long>(3 * k + 2) * w;
+      e2.out = sc.h;
+      e2.resid = sc.h;
+      e2.gate = sc.m + static_cast<long>(3 * k + 2) * w;
       e2.gate_ld = nm * w;
-      HEAD_HIP(gemm(hd->g, static_cast<const bf16_t*>(hd->fc2_w) + static_cast<long>(k) * w * w, R2, w, w, e2, st),
+      HEAD_HIP(gemm(sc.g, static_cast<const bf16_t*>(hd->fc2_w) + static_cast<long>(k) * w * w, R2, w, w, e2, st),
                "block second product");
     }
     float* tj = traj ? traj + static_cast<long>(j + 1) * R * T : nullptr;
     float* ej = eps_out ? eps_out + static_cast<long>(j) * R * T : nullptr;
-    HEAD_HIP(launch_out(hd, i, xi, R, scale, tj, ej, st), "output and sampler step");
+    HEAD_HIP(launch_out(hd, sc, i, xi, R, scale, tj, ej, st), "output and sampler step");
   }
-  HEAD_HIP(hipMemcpyAsync(x_out, hd->x, xbytes, hipMemcpyDeviceToDevice, st), "latent copy");
+  HEAD_HIP(hipMemcpyAsync(x_out, sc.x, xbytes, hipMemcpyDeviceToDevice, st), "latent copy");
+  return MAR_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Scratch of mar_head_sample_noalloc: one file-scope array per GPU, for
+// callers that cannot allocate device memory.  In host code `scratch` names
+// a host-side stand-in; the array's device address comes from
+// hipGetSymbolAddress, resolved once per device (at init, else at the
+// first call on that device) and kept in kScratchPtr.
+// ---------------------------------------------------------------------------
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array.
+mar_status static_scratch(void** out) {
+  int dev = -1;
+  HEAD_HIP(hipGetDevice(&dev), "current device");
+  if (dev < 0 || dev >= kMaxDevices) return hfail(MAR_E_DEVICE, "device %d beyond the scratch table", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HEAD_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "scratch address");
+    if (!p) return hfail(MAR_E_DEVICE, "scratch address is NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
   return MAR_OK;
 }
 
@@ -566,9 +640,19 @@ mar_status mar_head_init(const mar_head_dims* dims, const mar_head_weights* weig
                          size_t workspace_bytes, void* stream, mar_head** out) {
   abi_clear_error();
   try {
-    return head_init(dims, weights, workspace, workspace_bytes, stream, out);
+    mar_status s = head_init(dims, weights, workspace, workspace_bytes, stream, out);
+    if (s != MAR_OK) return s;
+    void* p = nullptr;
+    s = static_scratch(&p);  // the allocation-free entry point's array, resolved here once per device
+    if (s != MAR_OK) {
+      delete *out;
+      *out = nullptr;
+    }
+    return s;
   } catch (const std::bad_alloc&) {
     return hfail(MAR_E_HOST, "out of host memory");
+  } catch (const std::system_error&) {
+    return hfail(MAR_E_HOST, "lock failed");
   }
 }
 
@@ -577,8 +661,35 @@ mar_status mar_head_sample(mar_head* head, const float* y_cond, const float* y_u
                            const float* xi, float scale, float* x_out, float* trajectory, float* eps_out,
                            void* stream) {
   abi_clear_error();
-  return head_sample(head, y_cond, y_uncond, y_rows, row_cond, row_uncond, rows, x_init, xi, scale, x_out,
+  mar_status s = check_sample(head, y_cond, y_uncond, y_rows, row_cond, row_uncond, rows,
+                              head ? head->d.max_rows : 0, x_init, xi, scale, x_out, trajectory, eps_out);
+  if (s != MAR_OK || rows == 0) return s;
+  return head_sample(head, head->sc, y_cond, y_uncond, y_rows, row_cond, row_uncond, rows, x_init, xi, scale, x_out,
                      trajectory, eps_out, stream);
+}
+
+mar_status mar_head_sample_noalloc(mar_head* head, const float* y_cond, const float* y_uncond, int32_t y_rows,
+                                   const int32_t* row_cond, const int32_t* row_uncond, int32_t rows,
+                                   const float* x_init, const float* xi, float scale, float* x_out,
+                                   float* trajectory, float* eps_out, void* stream) {
+  abi_clear_error();
+  mar_status s = check_sample(head, y_cond, y_uncond, y_rows, row_cond, row_uncond, rows, 65536, x_init, xi, scale,
+                              x_out, trajectory, eps_out);
+  if (s != MAR_OK || rows == 0) return s;
+  size_t off[kScratchBuffers];
+  const size_t need = scratch_layout(head->d, static_cast<size_t>(rows), off);
+  if (need > kStaticScratchBytes)
+    return hfail(MAR_E_SHAPE, "%d rows need %zu bytes of scratch; the static array holds %zu", rows, need,
+                 kStaticScratchBytes);
+  void* base = nullptr;
+  try {
+    s = static_scratch(&base);
+  } catch (const std::system_error&) {
+    return hfail(MAR_E_HOST, "lock failed");
+  }
+  if (s != MAR_OK) return s;
+  return head_sample(head, scratch_at(static_cast<unsigned char*>(base), off), y_cond, y_uncond, y_rows, row_cond,
+                     row_uncond, rows, x_init, xi, scale, x_out, trajectory, eps_out, stream);
 }
 
 mar_status mar_head_destroy(mar_head* head) {
