@@ -127,12 +127,25 @@ __device__ __forceinline__ float silu_h(float x) {
   return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * x));
 }
 
+// in_w [w, T] (bf16) -> in_wt [T, w] (fp32), once at init, so that the
+// prologue reads four consecutive columns of one input component per load.
+__global__ void head_transpose_in_kernel(const bf16_t* __restrict__ in_w, int w, int T, float* __restrict__ in_wt) {
+  const long i = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= static_cast<long>(w) * T) return;
+  const int col = static_cast<int>(i / T), j = static_cast<int>(i - static_cast<long>(col) * T);
+  in_wt[static_cast<long>(j) * w + col] = bf2f(in_w[i]);
+}
+
 // Per sampling step, one wave per row r of the 2R: s[r] = silu(c[r] + e)
-// (bf16) and h[r] = b_in + W_in x[r mod R] (fp32).  in_w is [w, T] (bf16).
+// (bf16) and h[r] = b_in + W_in x[r mod R] (fp32), with in_wt = W_in^T
+// [T, w] in fp32.  TT = T when the token width is fixed at compile time
+// (16, KL-16 latents): the token's latent then sits in registers and every
+// weight load of a column group is issued before its multiply-adds.
+template <int TT>
 __global__ __launch_bounds__(256) void head_prologue_kernel(const float* __restrict__ c,
                                                             const float* __restrict__ e,
                                                             const float* __restrict__ x,
-                                                            const bf16_t* __restrict__ in_w,
+                                                            const float* __restrict__ in_wt,
                                                             const float* __restrict__ in_b, int R, int w, int T,
                                                             bf16_t* __restrict__ s, float* __restrict__ h) {
   const int lane = threadIdx.x & 63;
@@ -140,46 +153,112 @@ __global__ __launch_bounds__(256) void head_prologue_kernel(const float* __restr
   if (row >= 2 * R) return;
   const float* xr = x + static_cast<long>(row >= R ? row - R : row) * T;
   const long base = static_cast<long>(row) * w;
+  float xv[TT > 0 ? TT : 1];
+  if constexpr (TT > 0) {
+#pragma unroll
+    for (int j = 0; j < TT; j += 4) {
+      const f32x4_t q = *reinterpret_cast<const f32x4_t*>(xr + j);
+      xv[j] = q[0];
+      xv[j + 1] = q[1];
+      xv[j + 2] = q[2];
+      xv[j + 3] = q[3];
+    }
+  }
   for (int col = lane * 4; col < w; col += 256) {
     const f32x4_t cv = *reinterpret_cast<const f32x4_t*>(c + base + col);
     const f32x4_t ev = *reinterpret_cast<const f32x4_t*>(e + col);
+    f32x4_t hv = *reinterpret_cast<const f32x4_t*>(in_b + col);
+    if constexpr (TT > 0) {
+      f32x4_t wv[TT];
+#pragma unroll
+      for (int j = 0; j < TT; ++j) wv[j] = *reinterpret_cast<const f32x4_t*>(in_wt + static_cast<long>(j) * w + col);
+#pragma unroll
+      for (int j = 0; j < TT; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) hv[q] = fmaf(xv[j], wv[j][q], hv[q]);
+    } else {
+      for (int j = 0; j < T; ++j) {
+        const float xj = xr[j];
+        const f32x4_t wv = *reinterpret_cast<const f32x4_t*>(in_wt + static_cast<long>(j) * w + col);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) hv[q] = fmaf(xj, wv[q], hv[q]);
+      }
+    }
     *reinterpret_cast<u32x2_t*>(s + base + col) =
         u32x2_t{pack2bf(silu_h(cv[0] + ev[0]), silu_h(cv[1] + ev[1])), pack2bf(silu_h(cv[2] + ev[2]), silu_h(cv[3] + ev[3]))};
-    f32x4_t hv = *reinterpret_cast<const f32x4_t*>(in_b + col);
-    for (int j = 0; j < T; ++j) {
-      const float xj = xr[j];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) hv[q] = fmaf(xj, bf2f(in_w[static_cast<long>(col + q) * T + j]), hv[q]);
-    }
     *reinterpret_cast<f32x4_t*>(h + base + col) = hv;
   }
 }
 
-// Row statistics of a fp32 row held as groups of 4 per lane (w <= 256 G).
-template <int G>
+// Rows of the head are held 4 columns per lane per group: group k of lane
+// l is columns 4 l + 256 k .. + 3.  EXACT: the width is exactly 256 G, so
+// no group needs a bounds check (1024, 1280, 1536 = 256 x 4, 5, 6);
+// otherwise groups past the width are skipped.
+template <int G, bool EXACT>
+__device__ __forceinline__ bool group_in(int lane, int k, int w) {
+  return EXACT || lane * 4 + 256 * k < w;
+}
+
+__device__ __forceinline__ float bf_lo(uint32_t a) { return __uint_as_float(a << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t a) { return __uint_as_float(a & 0xFFFF0000u); }
+
+// Row statistics (mean, 1 / sqrt(var + eps)) of a row held in v.
+template <int G, bool EXACT>
 __device__ __forceinline__ void row_stats(const f32x4_t (&v)[G], int lane, int w, float eps, float& mean,
                                           float& rstd) {
   float sum = 0.f;
 #pragma unroll
-  for (int i = 0; i < G; ++i)
-    if (lane * 4 + 256 * i < w) sum += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
+  for (int k = 0; k < G; ++k)
+    if (group_in<G, EXACT>(lane, k, w)) sum += (v[k][0] + v[k][1]) + (v[k][2] + v[k][3]);
   mean = wave_sum(sum) / static_cast<float>(w);
   float sq = 0.f;
 #pragma unroll
-  for (int i = 0; i < G; ++i)
-    if (lane * 4 + 256 * i < w)
+  for (int k = 0; k < G; ++k)
+    if (group_in<G, EXACT>(lane, k, w))
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const float d = v[i][q] - mean;
+        const float d = v[k][q] - mean;
         sq = fmaf(d, d, sq);
       }
   rstd = __builtin_amdgcn_rsqf(wave_sum(sq) / static_cast<float>(w) + eps);
 }
 
+// v <- ln(v) (1 + scale) + shift for row `row` of h, with the shift and
+// scale at columns shift_off / scale_off of the modulation row mr.  Every
+// load (the row, then the shift and scale) is issued before the first
+// reduction.
+template <int G, bool EXACT>
+__device__ __forceinline__ void load_lnmod(const float* __restrict__ hrow, const bf16_t* __restrict__ mr,
+                                           int shift_off, int scale_off, int lane, int w, float eps,
+                                           f32x4_t (&v)[G]) {
+  u32x2_t sh[G], sc[G];
+#pragma unroll
+  for (int k = 0; k < G; ++k) {
+    const int col = lane * 4 + 256 * k;
+    if (group_in<G, EXACT>(lane, k, w)) {
+      v[k] = *reinterpret_cast<const f32x4_t*>(hrow + col);
+      sh[k] = *reinterpret_cast<const u32x2_t*>(mr + shift_off + col);
+      sc[k] = *reinterpret_cast<const u32x2_t*>(mr + scale_off + col);
+    } else {
+      v[k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      sh[k] = sc[k] = u32x2_t{0u, 0u};
+    }
+  }
+  float mean, rstd;
+  row_stats<G, EXACT>(v, lane, w, eps, mean, rstd);
+#pragma unroll
+  for (int k = 0; k < G; ++k) {
+    v[k][0] = fmaf((v[k][0] - mean) * rstd, 1.0f + bf_lo(sc[k][0]), bf_lo(sh[k][0]));
+    v[k][1] = fmaf((v[k][1] - mean) * rstd, 1.0f + bf_hi(sc[k][0]), bf_hi(sh[k][0]));
+    v[k][2] = fmaf((v[k][2] - mean) * rstd, 1.0f + bf_lo(sc[k][1]), bf_lo(sh[k][1]));
+    v[k][3] = fmaf((v[k][3] - mean) * rstd, 1.0f + bf_hi(sc[k][1]), bf_hi(sh[k][1]));
+  }
+}
+
 // u[r] = ln(h[r]) (1 + scale[r]) + shift[r] (bf16), one wave per row; the
 // shift and scale are columns [shift_off, +w) and [scale_off, +w) of the
-// modulation rows m [2R, ld] (bf16).
-template <int G>
+// modulation rows m [rows, ld] (bf16).
+template <int G, bool EXACT>
 __global__ __launch_bounds__(256) void head_lnmod_kernel(const float* __restrict__ h,
                                                          const bf16_t* __restrict__ m, int ld, int shift_off,
                                                          int scale_off, int rows, int w, float eps,
@@ -188,96 +267,106 @@ __global__ __launch_bounds__(256) void head_lnmod_kernel(const float* __restrict
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
   const long base = static_cast<long>(row) * w;
-  const bf16_t* mr = m + static_cast<long>(row) * ld;
   f32x4_t v[G];
+  load_lnmod<G, EXACT>(h + base, m + static_cast<long>(row) * ld, shift_off, scale_off, lane, w, eps, v);
 #pragma unroll
-  for (int i = 0; i < G; ++i) {
-    const int col = lane * 4 + 256 * i;
-    v[i] = col < w ? *reinterpret_cast<const f32x4_t*>(h + base + col) : f32x4_t{0.f, 0.f, 0.f, 0.f};
-  }
-  float mean, rstd;
-  row_stats<G>(v, lane, w, eps, mean, rstd);
-#pragma unroll
-  for (int i = 0; i < G; ++i) {
-    const int col = lane * 4 + 256 * i;
-    if (col >= w) continue;
-    const u32x2_t sh = *reinterpret_cast<const u32x2_t*>(mr + shift_off + col);
-    const u32x2_t sc = *reinterpret_cast<const u32x2_t*>(mr + scale_off + col);
-    float o[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t a = sh[q >> 1], b = sc[q >> 1];
-      const float shift = __uint_as_float((q & 1) ? (a & 0xFFFF0000u) : (a << 16));
-      const float scale = __uint_as_float((q & 1) ? (b & 0xFFFF0000u) : (b << 16));
-      o[q] = fmaf((v[i][q] - mean) * rstd, 1.0f + scale, shift);
-    }
-    *reinterpret_cast<u32x2_t*>(u + base + col) = u32x2_t{pack2bf(o[0], o[1]), pack2bf(o[2], o[3])};
+  for (int k = 0; k < G; ++k) {
+    const int col = lane * 4 + 256 * k;
+    if (group_in<G, EXACT>(lane, k, w))
+      *reinterpret_cast<u32x2_t*>(u + base + col) = u32x2_t{pack2bf(v[k][0], v[k][1]), pack2bf(v[k][2], v[k][3])};
   }
 }
 
-// One wave per token r: the final ln-modulation and output product of its
-// conditional row r and unconditional row R + r, the guided prediction
-// eps = eps_u + s (eps_c - eps_u), and the DDPM update of x[r] with the
-// coefficients of sampling step i and the draw xi_i[r] (not read when
-// sigma_i = 0).  Lane t < T owns component t.
-template <int G>
-__global__ __launch_bounds__(256) void head_out_kernel(const float* __restrict__ h,
+// One workgroup of two waves per token r: wave p takes row r + p R (p = 0
+// the conditional row, 1 the unconditional one): its final ln-modulation
+// and output product.  Then the guided prediction eps = eps_u + s (eps_c -
+// eps_u) and the DDPM update of x[r] with the coefficients of sampling step
+// i and the draw xi_i[r] (not read when sigma_i = 0).
+//
+// Each lane forms partial sums of all output components over its columns;
+// with T <= 16 they are summed across the wave by a reduce-scatter: four
+// halving exchanges (lane distance 32, 16, 8, 4) each keep half of the
+// components and add the partner's copy of that half, then two full
+// exchanges (distance 2, 1) complete the sum, leaving component
+// o = bits 5..2 of the lane in every lane of its group of four (a fixed
+// tree: deterministic).  Wider tokens take one wave reduction per
+// component.
+template <int G, bool EXACT>
+__global__ __launch_bounds__(128) void head_out_kernel(const float* __restrict__ h,
                                                        const bf16_t* __restrict__ m, int ld, int shift_off,
                                                        int scale_off, const bf16_t* __restrict__ out_w,
                                                        const float* __restrict__ out_b, const f32x4_t* __restrict__ coef,
                                                        int i, const float* __restrict__ xi, int R, int w, int T,
                                                        float eps_ln, float scale, float* __restrict__ x,
                                                        float* __restrict__ traj, float* __restrict__ eps_out) {
+  __shared__ float eps_sh[2][64];
   const int lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= R) return;
-  float e[2] = {0.f, 0.f};  // this lane's component of eps_c, eps_u
+  const int p = threadIdx.x >> 6;
+  const int r = blockIdx.x;
+  constexpr int TB = 16;  // components reduced by the butterfly
+  const long row = r + static_cast<long>(p) * R;
+  f32x4_t v[G];
+  load_lnmod<G, EXACT>(h + row * w, m + row * ld, shift_off, scale_off, lane, w, eps_ln, v);
+  if (T <= TB) {
+    float acc[TB];
 #pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    const long row = r + static_cast<long>(p) * R;
-    const bf16_t* mr = m + row * ld;
-    f32x4_t v[G];
+    for (int t = 0; t < TB; ++t) {
+      float part = 0.f;
+      if (t < T) {
+        u32x2_t wv[G];
 #pragma unroll
-    for (int k = 0; k < G; ++k) {
-      const int col = lane * 4 + 256 * k;
-      v[k] = col < w ? *reinterpret_cast<const f32x4_t*>(h + row * w + col) : f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int k = 0; k < G; ++k)
+          wv[k] = group_in<G, EXACT>(lane, k, w)
+                      ? *reinterpret_cast<const u32x2_t*>(out_w + static_cast<long>(t) * w + lane * 4 + 256 * k)
+                      : u32x2_t{0u, 0u};
+#pragma unroll
+        for (int k = 0; k < G; ++k) {
+          part = fmaf(v[k][0], bf_lo(wv[k][0]), part);
+          part = fmaf(v[k][1], bf_hi(wv[k][0]), part);
+          part = fmaf(v[k][2], bf_lo(wv[k][1]), part);
+          part = fmaf(v[k][3], bf_hi(wv[k][1]), part);
+        }
+      }
+      acc[t] = part;
     }
-    float mean, rstd;
-    row_stats<G>(v, lane, w, eps_ln, mean, rstd);
+    // reduce-scatter: after the exchange at distance d, lanes with that bit
+    // set hold the upper half of the remaining components
 #pragma unroll
-    for (int k = 0; k < G; ++k) {
-      const int col = lane * 4 + 256 * k;
-      if (col >= w) continue;
-      const u32x2_t sh = *reinterpret_cast<const u32x2_t*>(mr + shift_off + col);
-      const u32x2_t sc = *reinterpret_cast<const u32x2_t*>(mr + scale_off + col);
+    for (int half = TB / 2, d = 32; half >= 1; half >>= 1, d >>= 1) {
+      const bool up = (lane & d) != 0;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t a = sh[q >> 1], b = sc[q >> 1];
-        const float shift = __uint_as_float((q & 1) ? (a & 0xFFFF0000u) : (a << 16));
-        const float sca = __uint_as_float((q & 1) ? (b & 0xFFFF0000u) : (b << 16));
-        v[k][q] = fmaf((v[k][q] - mean) * rstd, 1.0f + sca, shift);
+      for (int k = 0; k < half; ++k) {
+        const float keep = up ? acc[k + half] : acc[k];
+        const float send = up ? acc[k] : acc[k + half];
+        acc[k] = keep + __shfl_xor(send, d, 64);
       }
     }
+    float tot = acc[0];
+    tot += __shfl_xor(tot, 2, 64);
+    tot += __shfl_xor(tot, 1, 64);
+    const int comp = (((lane >> 5) & 1) << 3) | (((lane >> 4) & 1) << 2) | (((lane >> 3) & 1) << 1) | ((lane >> 2) & 1);
+    if ((lane & 3) == 0 && comp < T) eps_sh[p][comp] = tot + out_b[comp];
+  } else {
     for (int t = 0; t < T; ++t) {
       float part = 0.f;
 #pragma unroll
       for (int k = 0; k < G; ++k) {
-        const int col = lane * 4 + 256 * k;
-        if (col >= w) continue;
-        const u32x2_t wv = *reinterpret_cast<const u32x2_t*>(out_w + static_cast<long>(t) * w + col);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const uint32_t a = wv[q >> 1];
-          part = fmaf(v[k][q], __uint_as_float((q & 1) ? (a & 0xFFFF0000u) : (a << 16)), part);
-        }
+        if (!group_in<G, EXACT>(lane, k, w)) continue;
+        const u32x2_t wv = *reinterpret_cast<const u32x2_t*>(out_w + static_cast<long>(t) * w + lane * 4 + 256 * k);
+        part = fmaf(v[k][0], bf_lo(wv[0]), part);
+        part = fmaf(v[k][1], bf_hi(wv[0]), part);
+        part = fmaf(v[k][2], bf_lo(wv[1]), part);
+        part = fmaf(v[k][3], bf_hi(wv[1]), part);
       }
       const float tot = wave_sum(part) + out_b[t];
-      if (lane == t) e[p] = tot;
+      if (lane == t) eps_sh[p][t] = tot;
     }
   }
-  if (lane < T) {
+  __syncthreads();
+  if (p == 0 && lane < T) {
     const f32x4_t cf = coef[i];
-    const float eg = fmaf(scale, e[0] - e[1], e[1]);
+    const float ec = eps_sh[0][lane], eu = eps_sh[1][lane];
+    const float eg = fmaf(scale, ec - eu, eu);
     const long at = static_cast<long>(r) * T + lane;
     const float xv = x[at];
     float nx = cf[0] * fmaf(-cf[1], eg, xv);
@@ -313,6 +402,7 @@ struct mar_head {
   // weights (matrices bf16, biases fp32)
   void *z_w, *t1_w, *t2_w, *in_w, *ada_w, *fc1_w, *fc2_w, *out_w;
   float *z_b, *t1_b, *t2_b, *in_b, *ada_b, *fc1_b, *fc2_b, *out_b;
+  float* in_wt;    // [T, w] the input product's weights, transposed, fp32
   float* e;        // [steps, w] time embeddings
   f32x4_t* coef;   // [steps] DDPM coefficients
   bf16_t* phi;     // [steps, freq] (init only)
@@ -377,14 +467,14 @@ HeadScratch scratch_at(unsigned char* base, const size_t* off) {
 // Byte offsets of the weights and tables in the workspace (in the order of
 // mar_head's fields), followed by the scratch for max_rows tokens at
 // off[kTables]; returns the total.
-constexpr int kTables = 20;
+constexpr int kTables = 21;
 size_t head_layout(const mar_head_dims& d, size_t* off) {
   const size_t w = d.width, D = d.cond_dim, T = d.token_dim, F = d.freq_dim, S = d.steps;
   const size_t nm = 3 * static_cast<size_t>(d.depth) + 2, L = d.depth;
   const size_t sizes[kTables] = {
       w * D * 2, w * F * 2, w * w * 2, w * T * 2, nm * w * w * 2, L * w * w * 2, L * w * w * 2, T * w * 2,
       w * 4, w * 4, w * 4, w * 4, nm * w * 4, L * w * 4, L * w * 4, T * 4,
-      S * w * 4, S * 16, S * F * 2, S * w * 2};
+      S * w * 4, S * 16, S * F * 2, S * w * 2, T * w * 4};
   size_t o = 0;
   for (int k = 0; k < kTables; ++k) {
     off[k] = o;
@@ -404,38 +494,52 @@ hipError_t launch_rows(Kern k, int rows, hipStream_t st, Args... args) {
 }
 
 // ln-modulation and output kernels by the groups of 4 a lane holds
-template <int G>
+template <int G, bool EXACT>
 hipError_t lnmod_as(const mar_head* hd, const HeadScratch& sc, int off_shift, int off_scale, int rows,
                     hipStream_t st) {
-  return launch_rows(head_lnmod_kernel<G>, rows, st, static_cast<const float*>(sc.h),
+  return launch_rows(head_lnmod_kernel<G, EXACT>, rows, st, static_cast<const float*>(sc.h),
                      static_cast<const bf16_t*>(sc.m), hd->n_mod * hd->d.width, off_shift, off_scale, rows,
                      hd->d.width, hd->d.ln_eps, sc.u);
 }
 hipError_t launch_lnmod(const mar_head* hd, const HeadScratch& sc, int off_shift, int off_scale, int rows,
                         hipStream_t st) {
+  switch (hd->d.width) {
+    case 1024: return lnmod_as<4, true>(hd, sc, off_shift, off_scale, rows, st);
+    case 1280: return lnmod_as<5, true>(hd, sc, off_shift, off_scale, rows, st);
+    case 1536: return lnmod_as<6, true>(hd, sc, off_shift, off_scale, rows, st);
+    default: break;
+  }
   const int G = (hd->d.width + 255) / 256;
-  if (G <= 2) return lnmod_as<2>(hd, sc, off_shift, off_scale, rows, st);
-  if (G <= 4) return lnmod_as<4>(hd, sc, off_shift, off_scale, rows, st);
-  if (G <= 8) return lnmod_as<8>(hd, sc, off_shift, off_scale, rows, st);
-  return lnmod_as<16>(hd, sc, off_shift, off_scale, rows, st);
+  if (G <= 2) return lnmod_as<2, false>(hd, sc, off_shift, off_scale, rows, st);
+  if (G <= 4) return lnmod_as<4, false>(hd, sc, off_shift, off_scale, rows, st);
+  if (G <= 8) return lnmod_as<8, false>(hd, sc, off_shift, off_scale, rows, st);
+  return lnmod_as<16, false>(hd, sc, off_shift, off_scale, rows, st);
 }
-template <int G>
+template <int G, bool EXACT>
 hipError_t out_as(const mar_head* hd, const HeadScratch& sc, int i, const float* xi, int R, float scale,
                   float* traj, float* eps_out, hipStream_t st) {
   const int w = hd->d.width;
-  return launch_rows(head_out_kernel<G>, R, st, static_cast<const float*>(sc.h), static_cast<const bf16_t*>(sc.m),
-                     hd->n_mod * w, 3 * hd->d.depth * w, (3 * hd->d.depth + 1) * w,
+  auto kern = head_out_kernel<G, EXACT>;
+  hipLaunchKernelGGL(kern, dim3(R), dim3(128), 0, st, static_cast<const float*>(sc.h),
+                     static_cast<const bf16_t*>(sc.m), hd->n_mod * w, 3 * hd->d.depth * w, (3 * hd->d.depth + 1) * w,
                      static_cast<const bf16_t*>(hd->out_w), static_cast<const float*>(hd->out_b),
                      static_cast<const f32x4_t*>(hd->coef), i, xi, R, w, hd->d.token_dim, hd->d.ln_eps, scale, sc.x,
                      traj, eps_out);
+  return hipGetLastError();
 }
 hipError_t launch_out(const mar_head* hd, const HeadScratch& sc, int i, const float* xi, int R, float scale,
                       float* traj, float* eps_out, hipStream_t st) {
+  switch (hd->d.width) {
+    case 1024: return out_as<4, true>(hd, sc, i, xi, R, scale, traj, eps_out, st);
+    case 1280: return out_as<5, true>(hd, sc, i, xi, R, scale, traj, eps_out, st);
+    case 1536: return out_as<6, true>(hd, sc, i, xi, R, scale, traj, eps_out, st);
+    default: break;
+  }
   const int G = (hd->d.width + 255) / 256;
-  if (G <= 2) return out_as<2>(hd, sc, i, xi, R, scale, traj, eps_out, st);
-  if (G <= 4) return out_as<4>(hd, sc, i, xi, R, scale, traj, eps_out, st);
-  if (G <= 8) return out_as<8>(hd, sc, i, xi, R, scale, traj, eps_out, st);
-  return out_as<16>(hd, sc, i, xi, R, scale, traj, eps_out, st);
+  if (G <= 2) return out_as<2, false>(hd, sc, i, xi, R, scale, traj, eps_out, st);
+  if (G <= 4) return out_as<4, false>(hd, sc, i, xi, R, scale, traj, eps_out, st);
+  if (G <= 8) return out_as<8, false>(hd, sc, i, xi, R, scale, traj, eps_out, st);
+  return out_as<16, false>(hd, sc, i, xi, R, scale, traj, eps_out, st);
 }
 
 hipError_t fill_zero(float* p, long n, hipStream_t st) {
@@ -479,6 +583,7 @@ mar_status head_init(const mar_head_dims* dims, const mar_head_weights* W, void*
   hd->coef = reinterpret_cast<f32x4_t*>(ws + off[17]);
   hd->phi = reinterpret_cast<bf16_t*>(ws + off[18]);
   hd->t1o = reinterpret_cast<bf16_t*>(ws + off[19]);
+  hd->in_wt = reinterpret_cast<float*>(ws + off[20]);
   size_t soff[kScratchBuffers];
   scratch_layout(d, static_cast<size_t>(d.max_rows), soff);
   hd->sc = scratch_at(ws + off[kTables], soff);
@@ -512,6 +617,12 @@ mar_status head_init(const mar_head_dims* dims, const mar_head_weights* W, void*
   e2.out = hd->e;
   e2.resid = hd->e;
   HEAD_HIP(gemm(hd->t1o, hd->t2_w, d.steps, d.width, d.width, e2, st), "time embedding (second product)");
+  {
+    const long n = static_cast<long>(d.width) * d.token_dim;
+    hipLaunchKernelGGL(head_transpose_in_kernel, dim3((n + 255) / 256), dim3(256), 0, st,
+                       static_cast<const bf16_t*>(hd->in_w), d.width, d.token_dim, hd->in_wt);
+    HEAD_HIP(hipGetLastError(), "input weights");
+  }
   *out = hd.release();
   return MAR_OK;
 }
@@ -559,9 +670,10 @@ mar_status head_sample(const mar_head* hd, const HeadScratch& sc, const float* y
   if (traj) HEAD_HIP(hipMemcpyAsync(traj, x_init, xbytes, hipMemcpyDeviceToDevice, st), "trajectory copy");
   for (int j = 0; j < d.steps; ++j) {
     const int i = d.steps - 1 - j;
-    HEAD_HIP(launch_rows(head_prologue_kernel, R2, st, static_cast<const float*>(sc.c),
+    HEAD_HIP(launch_rows(T == 16 ? head_prologue_kernel<16> : head_prologue_kernel<0>, R2, st,
+                         static_cast<const float*>(sc.c),
                          static_cast<const float*>(hd->e + static_cast<long>(i) * w), static_cast<const float*>(sc.x),
-                         static_cast<const bf16_t*>(hd->in_w), static_cast<const float*>(hd->in_b), static_cast<int>(R),
+                         static_cast<const float*>(hd->in_wt), static_cast<const float*>(hd->in_b), static_cast<int>(R),
                          w, T, sc.s, sc.h),
              "prologue");
     EpiArgs em{};
