@@ -57,8 +57,12 @@ def parse():
     ap.add_argument("--steps", type=int, default=3, help="timed schedules")
     ap.add_argument("--warmup", type=int, default=1, help="untimed schedules")
     ap.add_argument("--workload", default="mar-l", choices=["mar-l", "mar-b", "mar-h", "mar-l-hires"])
-    ap.add_argument("--profile-kind", default="fc1", choices=list(KIND_ROOFLINE),
-                    help="kernel class timed with HIP events for the roofline")
+    ap.add_argument("--profile-kind", default="fc2", choices=list(KIND_ROOFLINE),
+                    help="kernel class timed with HIP events for the roofline (default: fc2, the class with "
+                         "the most GPU time in the MAR-L schedule)")
+    ap.add_argument("--no-classes", action="store_true",
+                    help="skip the per-class table (one extra schedule per kernel class, each class timed "
+                         "with HIP events against its own roof)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--schedule", default="64", choices=list(SCHEDULES),
                     help="the paper's settings: 64 decoding steps (start 5, tau 9) or 32 (start 4, tau 5)")
@@ -79,6 +83,9 @@ def parse():
     ap.add_argument("--memory-shapes", action="store_true",
                     help="only run the memory-bound kernels (LayerNorm dense and gather, scores, select) once "
                          "each at the MAR-L schedule's shapes (for hardware-counter runs)")
+    ap.add_argument("--no-head", action="store_true",
+                    help="skip the diffusion-head leg (the per-token head run for the tokens each decoding "
+                         "step decodes, timed beside the transformer schedule)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (the reference "
                          "dispatch that scales the HBM byte counters) and exit")
@@ -86,7 +93,7 @@ def parse():
 
 
 COPY_BYTES = 1 << 30
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fc1_hbm_traffic_mar_l.md")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "{kind}_hbm_traffic_mar_l.md")
 GEMM_SOURCE = os.path.join(ROOT, "paper_2503_12450_amd", "csrc", "gemm.hip")
 
 
@@ -210,12 +217,13 @@ def memory_shapes():
     print(json.dumps({"memory_launches": launches}), flush=True)
 
 
-def recorded_traffic():
-    """HBM bytes per fc1 launch from the committed counter runs, or None when
-    the GEMM source changed since they were taken."""
+def recorded_traffic(kind):
+    """HBM bytes per launch of a product class from the committed counter
+    runs, or None when there are none or the GEMM source changed since they
+    were taken."""
     import hashlib
     try:
-        text = open(TRAFFIC_FILE).read()
+        text = open(TRAFFIC_FILE.format(kind=kind)).read()
         src = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
     except OSError:
         return None
@@ -312,6 +320,81 @@ def given_rows(rule, recipe, plans, slots, seq, n):
         t = torch.from_numpy(rows).pin_memory()
         out[i] = (t, t.numpy())
     return out
+
+
+def head_leg(args, wl, dims, recipe, plans, cache, X, n, images, scale, dev):
+    """One schedule with the diffusion head after every decoding step: the
+    tokens decoded at that step (the cosine schedule) are sampled over 100
+    DDPM steps, conditioned on their rows of the output cache (conditional
+    slots) and on the unconditional rows of the same step (the output cache
+    on two-pathway steps, the condition cache's reconstruction on reuse
+    steps).  Timed with HIP events around the head calls; the transformer
+    work between them runs as in the headline schedule."""
+    import numpy as np
+    import torch
+
+    from paper_2503_12450_amd import binding as B
+    from paper_2503_12450_amd import schedule as sch
+    from paper_2503_12450_amd.device import upload_head
+    from paper_2503_12450_amd.workload import BUFFER_ROWS, HEADS, decoded_at, head_weights
+    from paper_2503_12450_amd.flops import head_flops_per_eval
+
+    key = {"mar-l": "mar-l", "mar-b": "mar-b", "mar-h": "mar-h", "mar-l-hires": "mar-l"}[args.workload]
+    S, D = dims.seq_len, dims.d_model
+    per_step = [decoded_at(recipe, k) for k in range(len(plans))]
+    R_max = max(r.size for r in per_step)
+    from dataclasses import replace
+    hd = replace(HEADS[key], cond_dim=D, max_rows=R_max)
+    head = B.MarHead(hd, upload_head(head_weights(hd), hd.dtype, device=dev))
+    rows = []
+    for r in per_step:
+        flat = (np.arange(images)[:, None] * S + BUFFER_ROWS + r).reshape(-1).astype(np.int32)
+        rows.append(torch.from_numpy(flat).to(dev))
+    g = torch.Generator(device=dev).manual_seed(5)
+    x0 = [torch.randn(r.size, hd.token_dim, device=dev, generator=g) for r in per_step]
+    xi = [torch.randn(hd.steps, r.size, hd.token_dim, device=dev, generator=g) for r in per_step]
+    xo = [torch.empty(r.size, hd.token_dim, device=dev) for r in per_step]
+    Y = cache.output()
+    u_hat = torch.empty((images, S, D), dtype=torch.float32, device=dev)
+    guided = torch.empty((images, S, D), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+
+    def run(events=None):
+        for i, p in enumerate(plans):
+            slots = 2 * images if p.branches == sch.BOTH else images
+            if p.mode == sch.FULL:
+                cache.step(X[i], B.MAR_FULL)
+            else:
+                cache.step(X[i][:slots], B.MAR_TOKEN_CACHED, n, slot0=0)
+            if p.cfg == sch.STORE:
+                cache.cfg_combine(B.MAR_CFG_STORE, Y[:images], Y[images:2 * images], scale, guided)
+                y_unc = Y[images:2 * images]
+            else:
+                cache.cfg_combine(B.MAR_CFG_REUSE, Y[:images], None, scale, guided, u_hat)
+                y_unc = u_hat
+            if events is not None:
+                events[i][0].record()
+            head.sample(Y[:images], y_unc, rows[i], rows[i], x0[i], xi[i], scale, xo[i])
+            if events is not None:
+                events[i][1].record()
+
+    run()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in plans]
+    t0 = time.perf_counter()
+    run(ev)
+    torch.cuda.synchronize()
+    wall_ms = 1e3 * (time.perf_counter() - t0)
+    head_ms = sum(a.elapsed_time(b) for a, b in ev)
+    tokens = sum(r.size for r in per_step)
+    fl = head_flops_per_eval(hd) * 2 * tokens * hd.steps
+    return {
+        "what": (f"per-token diffusion head (width {hd.width}, {hd.depth} blocks, {hd.steps} DDPM steps, both "
+                 f"guidance branches) on the {tokens} tokens the {len(plans)}-step schedule decodes"),
+        "schedule_with_head_ms": wall_ms, "head_ms": head_ms, "head_share": head_ms / wall_ms,
+        "head_tflops": fl / (head_ms / 1e3) / 1e12, "head_frac_of_bf16_peak": fl / (head_ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
+        "tokens": tokens, "max_tokens_per_step": R_max,
+    }
 
 
 def main():
@@ -435,7 +518,7 @@ def main():
         "kernel": what,
         "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
         "frac": (achieved / peak) if achieved else None,
-        "traffic": recorded_traffic() if args.profile_kind == "fc1" and args.workload == "mar-l" else None,
+        "traffic": recorded_traffic(args.profile_kind) if args.workload == "mar-l" else None,
         "launches": prof_n, "avg_launch_us": 1e3 * prof_ms / max(prof_n, 1),
         "flops_per_launch": prof_flops / max(prof_n, 1),
         "bytes_per_launch": prof_bytes / max(prof_n, 1),
@@ -458,6 +541,27 @@ def main():
         "speedup_cached_cond_vs_full": (mean["full"] / mean["cached_cond"]) if mean["cached_cond"] else None,
         "roofline": roofline,
     }
+    if not args.no_classes:
+        classes = {}
+        for kind, (what_k, bound_k) in KIND_ROOFLINE.items():
+            cache.profile_start(kind)
+            schedule_run()
+            torch.cuda.synchronize()
+            ms_k, n_k, fl_k, by_k = cache.profile_stop()
+            ach = (fl_k if bound_k == "mfma" else by_k) / (ms_k / 1e3) / (1e12 if bound_k == "mfma" else 1e9) \
+                if ms_k > 0 else None
+            pk = PEAK_BF16_TFLOPS if bound_k == "mfma" else PEAK_HBM_GBS
+            classes[kind] = {"bound": bound_k, "ms_per_schedule": ms_k, "launches": n_k,
+                             "avg_launch_us": 1e3 * ms_k / max(n_k, 1), "achieved": ach,
+                             "unit": "TFLOP/s" if bound_k == "mfma" else "GB/s",
+                             "frac": (ach / pk) if ach else None}
+        total_k = sum(c["ms_per_schedule"] for c in classes.values())
+        for c in classes.values():
+            c["share_of_kernel_time"] = c["ms_per_schedule"] / total_k if total_k else None
+        line["kernel_classes"] = classes
+        line["dominant_class"] = max(classes, key=lambda k: classes[k]["ms_per_schedule"])
+    if not args.no_head and args.rule == "least":
+        line["diffusion_head"] = head_leg(args, wl, dims, recipe, plans, cache, X, n, images, scale, dev)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(dims, W, recipe, n, plans)
     print(json.dumps(line), flush=True)

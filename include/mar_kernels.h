@@ -111,7 +111,7 @@ mar_status mar_k_select_most_similar(const double* scores, int32_t n_slots, int3
  * choice by shape.  Every configuration uses the same MFMA instruction and
  * visits k in the same order, so results do not change by a single bit.
  * Not thread-safe with concurrent launches. */
-#define MAR_GEMM_VARIANTS 14
+#define MAR_GEMM_VARIANTS 16
 mar_status mar_k_gemm_variant(int32_t variant);
 
 #ifdef __cplusplus

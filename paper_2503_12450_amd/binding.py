@@ -35,7 +35,7 @@ EXPORTED = (
     "mar_head_workspace_bytes", "mar_head_init", "mar_head_sample", "mar_head_destroy",
     "mar_head_sample_noalloc",
 )
-GEMM_VARIANTS = 14
+GEMM_VARIANTS = 16
 
 
 class MarError(RuntimeError):

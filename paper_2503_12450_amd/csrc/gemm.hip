@@ -784,30 +784,37 @@ static hipError_t gemm_pick(const void* A, const void* W, int M, int N, int K, c
     // tiles with a two-stage ring of 128-byte slices, launched persistent
     // once there are several tiles per CU.  Products too small to give
     // even 128 tiles of 128 x 128 (the diffusion head's, a few hundred
-    // rows) take 64 x 64 tiles, four times as many workgroups.
+    // rows) take 64 x 64 tiles, four times as many workgroups; at most 256
+    // tiles of 128 x 128 with the fp32 residual epilogue (the cached
+    // blocks' projections at 3200 rows) run eight waves per tile; very wide
+    // products on few rows (the head's modulation product, N = 33280 on
+    // under 2048 rows) run persistent 128 x 128 tiles, two per CU.
     const long big = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
     const long small = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
     if (small < 128)
       v = 6;
     else if (small <= 256)
-      v = 1;
+      v = kResid ? 7 : 1;
+    else if (N >= 8192 && M <= 2048)
+      v = 12;
     else if (kResid)
-      v = big <= 512 ? 4 : 7;
+      v = big <= 512 ? 4 : 8;
     else if (big <= 512)
       v = kAct || big <= 256 ? 0 : 4;
     else
-      v = big <= 1280 ? 0 : 7;
+      v = big <= 1280 ? 0 : 8;
   }
-  // variants 7..13: the configurations of 0..6 launched persistent
-  const bool persist = v >= 7;
-  if (persist) v -= 7;
+  // variants 8..15: the configurations of 0..7 launched persistent
+  const bool persist = v >= 8;
+  if (persist) v -= 8;
   // a ring needs a minimum number of slices per tile (two for the two-stage
   // rings, which load two slices ahead; S-1 for S stages): short K takes
   // 128 x 128 tiles with 64-byte slices (K * sizeof(T) is a multiple of 128)
-  static const int kMinSlices[7] = {2, 2, 2, 2, 2, 3, 2}, kRowB[7] = {128, 128, 128, 128, 128, 64, 128};
-  if (K * static_cast<int>(sizeof(T)) / kRowB[v] < kMinSlices[v]) v = 7;
+  static const int kMinSlices[8] = {2, 2, 2, 2, 2, 3, 2, 2}, kRowB[8] = {128, 128, 128, 128, 128, 64, 128, 128};
+  if (K * static_cast<int>(sizeof(T)) / kRowB[v] < kMinSlices[v]) v = 8;
   switch (v) {
-    case 7: return gemm_launch<T, 128, 128, 2, 2, 2, 64, KIND>(A, W, M, N, K, e, persist, st);
+    case 8: return gemm_launch<T, 128, 128, 2, 2, 2, 64, KIND>(A, W, M, N, K, e, persist, st);
+    case 7: return gemm_launch<T, 128, 128, 2, 4, 3, 128, KIND>(A, W, M, N, K, e, persist, st);
     case 0: return gemm_launch<T, 256, 256, 2, 4, 2, 128, KIND>(A, W, M, N, K, e, persist, st);
     case 1: return gemm_launch<T, 128, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);
     case 2: return gemm_launch<T, 256, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);

@@ -31,3 +31,12 @@ def gemm_launch_flops(M: int, N: int, K: int) -> int:
 def gemm_launch_bytes(M: int, N: int, K: int, es: int, out_es: int, resid: bool = False) -> int:
     """Operands read once, output written once (+ residual read)."""
     return (M * K + N * K) * es + M * N * out_es + (M * N * 4 if resid else 0)
+
+
+def head_flops_per_eval(hd) -> int:
+    """One evaluation of the diffusion head for one row: the input product,
+    the modulation product of every block and the final layer, the blocks'
+    two products and the output product (the conditioning product and the
+    time embedding run once per call and are not counted per evaluation)."""
+    w, T = hd.width, hd.token_dim
+    return 2 * (T * w + (3 * hd.depth + 2) * w * w + 2 * hd.depth * w * w + w * T)

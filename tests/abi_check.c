@@ -78,7 +78,7 @@ int main(void) {
   CHECK(mar_k_select_most_similar(NULL, 1, 8, 2, NULL, NULL) == MAR_E_ARG);
   CHECK(mar_cache_destroy(NULL) == MAR_OK);
   CHECK(mar_output(NULL) == NULL);
-  CHECK(mar_k_gemm_variant(14) == MAR_E_ARG);
+  CHECK(mar_k_gemm_variant(16) == MAR_E_ARG);
   CHECK(mar_k_gemm_variant(-1) == MAR_OK);
 
   /* the diffusion head: sizing and host-side checks */

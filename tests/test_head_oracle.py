@@ -40,6 +40,12 @@ def test_head_size_reproduces_table1_constant():
         assert abs(head / const - 1) < 0.05, (model, head, const)
 
 
+def test_benchmark_counts_the_head_like_the_oracle():
+    from paper_2503_12450_amd.flops import head_flops_per_eval
+    for hd in HEADS.values():
+        assert head_flops_per_eval(hd) == DH.head_flops_per_eval(hd)
+
+
 def test_silu_and_plain_layer_norm_match_torch():
     x = np.random.default_rng(0).standard_normal((6, 40)) * 3
     np.testing.assert_allclose(DH.silu(x), torch.nn.functional.silu(torch.from_numpy(x)).numpy(),
