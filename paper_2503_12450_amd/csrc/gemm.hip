@@ -769,9 +769,48 @@ static hipError_t gemm_launch(const void* A, const void* W, int M, int N, int K,
 // same order, so the choice never changes a result bit.
 int g_gemm_variant = -1;  // test hook: force a variant (-1 = by shape)
 
+// Persistent 256 x 256 launches whose last round of tiles would leave CUs
+// idle: the whole rounds keep the 256 x 256 tiles (rows [0, M1)), and the
+// rows left over go to a second launch of 256 x 128 tiles, at most one per
+// CU, so that no CU runs a last round alone (M = 40960, N = 1024: 640 tiles
+// on 256 CUs would take three rounds; 512 tiles and then 256 half-size
+// tiles take about 2.6).  Each output row belongs to one tile of one launch
+// and every configuration sums k in the same order: the bits do not change.
+// Only for epilogues whose rows map one to one onto the output rows.
+template <typename T, int KIND>
+static hipError_t gemm_balanced(const void* A, const void* W, int M, int N, int K, const EpiArgs& e,
+                                hipStream_t st) {
+  constexpr bool kRowMapped = KIND == EPI_BIAS || KIND == EPI_GELU || KIND == EPI_SILU || KIND == EPI_GATE ||
+                              KIND == EPI_RESIDUAL;
+  const int cus = device_cus();
+  const long tn = (N + 255) / 256;
+  const long tiles = static_cast<long>((M + 255) / 256) * tn;
+  const long rounds = tiles / cus, rem = tiles - rounds * cus;
+  const long m1_tiles = rounds * cus / tn;
+  const int M1 = static_cast<int>(m1_tiles * 256), M2 = M - M1;
+  const long tiles2 = static_cast<long>((M2 + 255) / 256) * ((N + 127) / 128);
+  const bool split = kRowMapped && !(KIND == EPI_RESIDUAL && (e.out_idx || e.resid_copy)) && rounds > 0 &&
+                     rem > 0 && M1 > 0 && M2 > 0 && tiles2 <= cus;
+  if (!split) return gemm_launch<T, 256, 256, 2, 4, 2, 128, KIND>(A, W, M, N, K, e, true, st);
+  hipError_t err = gemm_launch<T, 256, 256, 2, 4, 2, 128, KIND>(A, W, M1, N, K, e, true, st);
+  if (err != hipSuccess) return err;
+  EpiArgs e2 = e;
+  const size_t off = static_cast<size_t>(M1) * N;
+  if constexpr (KIND == EPI_RESIDUAL || KIND == EPI_GATE) {
+    e2.out = static_cast<float*>(e.out) + off;
+    e2.resid = e.resid + off;
+    if constexpr (KIND == EPI_GATE) e2.gate = static_cast<const T*>(e.gate) + static_cast<size_t>(M1) * e.gate_ld;
+  } else {
+    e2.out = static_cast<T*>(e.out) + off;
+  }
+  const void* A2 = static_cast<const T*>(A) + static_cast<size_t>(M1) * K;
+  return gemm_launch<T, 256, 128, 2, 2, 3, 128, KIND>(A2, W, M2, N, K, e2, false, st);
+}
+
 template <typename T, int KIND>
 static hipError_t gemm_pick(const void* A, const void* W, int M, int N, int K, const EpiArgs& e,
                             hipStream_t st) {
+  const bool by_shape = g_gemm_variant < 0;
   constexpr bool kResid = KIND == EPI_RESIDUAL || KIND == EPI_GATE;
   constexpr bool kAct = KIND == EPI_GELU || KIND == EPI_SILU;
   int v = g_gemm_variant;
@@ -815,7 +854,9 @@ static hipError_t gemm_pick(const void* A, const void* W, int M, int N, int K, c
   switch (v) {
     case 8: return gemm_launch<T, 128, 128, 2, 2, 2, 64, KIND>(A, W, M, N, K, e, persist, st);
     case 7: return gemm_launch<T, 128, 128, 2, 4, 3, 128, KIND>(A, W, M, N, K, e, persist, st);
-    case 0: return gemm_launch<T, 256, 256, 2, 4, 2, 128, KIND>(A, W, M, N, K, e, persist, st);
+    case 0:
+      if (persist && by_shape) return gemm_balanced<T, KIND>(A, W, M, N, K, e, st);
+      return gemm_launch<T, 256, 256, 2, 4, 2, 128, KIND>(A, W, M, N, K, e, persist, st);
     case 1: return gemm_launch<T, 128, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);
     case 2: return gemm_launch<T, 256, 128, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);
     case 3: return gemm_launch<T, 128, 256, 2, 2, 3, 128, KIND>(A, W, M, N, K, e, persist, st);

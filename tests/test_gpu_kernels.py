@@ -154,6 +154,41 @@ def test_persistent_workgroups_walk_several_tiles(dtype, variant):
     _close(out[torch.from_numpy(rows).to(DEV)], want, dtype)
 
 
+@pytest.mark.parametrize("kind,M,N", [("residual", 33280, 1024), ("gelu", 41216, 2048)])
+def test_balanced_last_round_is_bitwise_identical(kind, M, N):
+    """By shape, a persistent 256 x 256 launch whose last round would leave
+    CUs idle runs its whole rounds with 256 x 256 tiles and the rows left
+    over with 256 x 128 tiles (a second launch).  Same bits as one
+    workgroup per 256 x 256 tile, and within tolerance of the oracle on rows
+    of both parts."""
+    K = 256
+    a_h = normal_rows((M, K), seed=81, dtype="bf16")
+    w_h = normal_rows((N, K), seed=82, std=0.05, dtype="bf16")
+    bias_h = normal_rows((N,), seed=83)
+    a, w, bias = to_device(a_h, "bf16"), to_device(w_h, "bf16"), to_device(bias_h, "f32")
+    if kind == "residual":
+        r_h = normal_rows((M, N), seed=84)
+        ref, out = to_device(r_h, "f32"), to_device(r_h, "f32")
+        run = lambda o: B.k_linear_residual("bf16", a, w, bias, o, o)  # noqa: E731
+    else:
+        ref = torch.empty((M, N), dtype=torch.bfloat16, device=DEV)
+        out = torch.empty_like(ref)
+        run = lambda o: B.k_linear("bf16", a, w, bias, o, gelu=True)  # noqa: E731
+    try:
+        B.k_gemm_variant(0)
+        run(ref)
+        B.k_gemm_variant(-1)
+        run(out)
+    finally:
+        B.k_gemm_variant(-1)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
+    rows = np.array([0, 255, 32767, 32768, M - 257, M - 1])
+    want = O.linear(a_h[rows], w_h, bias_h)
+    want = want + r_h[rows] if kind == "residual" else O.gelu(want)
+    _close(out[torch.from_numpy(rows).to(DEV)], want, "bf16")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("M,N,K", [(200, 256, 512), (200, 264, 128)])
 def test_linear_residual_in_place_and_scatter(dtype, M, N, K):
