@@ -17,7 +17,7 @@ cached step, so N = 70).
 Other options: --workload (the MAR-B, MAR-H and 1088-token shapes), --rule
 (the selection strategies of the paper's comparison), --score-source and
 --fresh-kv (the method's variants), --profile-kind (which kernel class the
-roofline reports, against the MFMA or the HBM peak).  --fc1-shapes,
+roofline reports, against the MFMA or the HBM peak).  --gemm-shapes,
 --attention-shapes, --memory-shapes and --calibrate-copy only run single
 launches for hardware-counter passes.
 
@@ -73,8 +73,8 @@ def parse():
     ap.add_argument("--rule", default="least", choices=list(RULES),
                     help="token selection of the cached steps (Table 3): least / most similar on the "
                          "device, or random / token-type rows chosen on the host")
-    ap.add_argument("--fc1-shapes", action="store_true",
-                    help="only run the fc1 product once per shape the 64-step MAR-L schedule "
+    ap.add_argument("--gemm-shapes", default=None, choices=["qkv", "proj", "fc1", "fc2"],
+                    help="only run one product class once per shape the 64-step MAR-L schedule "
                          "launches (for hardware-counter runs) and print each shape's launches per "
                          "schedule")
     ap.add_argument("--attention-shapes", action="store_true",
@@ -108,10 +108,13 @@ def calibrate_copy():
     print(json.dumps({"copy_bytes": COPY_BYTES, "dispatches": 3}), flush=True)
 
 
-def fc1_shapes():
-    """The fc1 products of one 64-step MAR-L schedule: rows M -> launches.  Full steps run
-    every block on every row of both pathways; cached steps the prefix
-    blocks on every row and the rest on N rows per sequence."""
+def gemm_shapes(kind):
+    """One product class of the 64-step MAR-L schedule, once per row count
+    it launches: rows M -> launches per schedule.  Full steps run every
+    block on every row of both pathways; cached steps the prefix blocks on
+    every row and the rest on N rows per sequence.  Each launch goes through
+    the class's own entry point and epilogue (QKV with the key/value cache
+    scatter, fc1 with GELU, proj and fc2 with the fp32 residual)."""
     import torch
 
     from paper_2503_12450_amd import binding as B
@@ -120,24 +123,40 @@ def fc1_shapes():
 
     wl = WORKLOADS["mar-l"]
     d, n, img = wl.dims, wl.n_recompute, wl.images
+    D, F, S, H = d.d_model, d.d_mlp, d.seq_len, d.n_heads
+    N, K = {"qkv": (3 * D, D), "proj": (D, D), "fc1": (F, D), "fc2": (D, F)}[kind]
     counts = {}
     n_steps, start, tau, _ = SCHEDULES["64"]
     for p in sch.lazymar_schedule(n_steps, start, tau, "alternate"):
         seqs = 2 * img if (p.mode == sch.FULL or p.branches == sch.BOTH) else img
         if p.mode == sch.FULL:
-            counts[seqs * d.seq_len] = counts.get(seqs * d.seq_len, 0) + d.n_layers
+            counts[seqs * S] = counts.get(seqs * S, 0) + d.n_layers
         else:
-            counts[seqs * d.seq_len] = counts.get(seqs * d.seq_len, 0) + d.full_prefix
+            counts[seqs * S] = counts.get(seqs * S, 0) + d.full_prefix
             counts[seqs * n] = counts.get(seqs * n, 0) + d.n_layers - d.full_prefix
-    g = torch.Generator(device="cuda:0").manual_seed(0)
-    w = (torch.randn(d.d_mlp, d.d_model, device="cuda:0", generator=g) * 0.02).to(torch.bfloat16)
-    bias = torch.zeros(d.d_mlp, device="cuda:0")
+    dev = "cuda:0"
+    g = torch.Generator(device=dev).manual_seed(0)
+    w = (torch.randn(N, K, device=dev, generator=g) * 0.02).to(torch.bfloat16)
+    bias = torch.zeros(N, device=dev)
     for m in sorted(counts, reverse=True):
-        a = torch.randn(m, d.d_model, device="cuda:0", generator=g).to(torch.bfloat16)
-        out = torch.empty(m, d.d_mlp, device="cuda:0", dtype=torch.bfloat16)
-        B.k_linear("bf16", a, w, bias, out, gelu=True)
+        a = torch.randn(m, K, device=dev, generator=g).to(torch.bfloat16)
+        per = S if m in (2 * img * S, img * S) else n   # dense rows: whole sequences
+        seqs = m // per
+        if kind == "qkv":
+            q = torch.empty(m, D, device=dev, dtype=torch.bfloat16)
+            kc = torch.empty(seqs, H, S, D // H, device=dev, dtype=torch.bfloat16)
+            vc = torch.empty_like(kc)
+            idx = None if per == S else torch.stack(
+                [torch.randperm(S, device=dev, generator=g)[:per].sort().values for _ in range(seqs)]).to(torch.int32)
+            B.k_qkv("bf16", a, w, bias, D, H, S, per, q_out=q, k_cache=kc, v_cache=vc, idx=idx)
+        elif kind == "fc1":
+            out = torch.empty(m, N, device=dev, dtype=torch.bfloat16)
+            B.k_linear("bf16", a, w, bias, out, gelu=True)
+        else:
+            r = torch.randn(m, N, device=dev, generator=g)
+            B.k_linear_residual("bf16", a, w, bias, r, r)
     torch.cuda.synchronize()
-    print(json.dumps({"fc1_rows_to_launches_per_schedule": counts, "n": d.d_mlp, "k": d.d_model}), flush=True)
+    print(json.dumps({f"{kind}_rows_to_launches_per_schedule": counts, "n": N, "k": K}), flush=True)
 
 
 def attention_shapes():
@@ -402,8 +421,8 @@ def main():
     if args.calibrate_copy:
         calibrate_copy()
         return
-    if args.fc1_shapes:
-        fc1_shapes()
+    if args.gemm_shapes:
+        gemm_shapes(args.gemm_shapes)
         return
     if args.attention_shapes:
         attention_shapes()

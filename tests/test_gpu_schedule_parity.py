@@ -19,10 +19,12 @@ those near-equal tokens are picked is not fixed by the method.  Hence:
   same step: every selected token scores at most threshold + band and every
   other token at least threshold - band, with threshold the oracle's N-th
   smallest score and band = 4 x the largest score change that storage
-  rounding alone causes on that slot (oracle.storage_emulation over the
-  always-computed blocks); on a slot whose threshold gap exceeds 2 x band
-  the sets must be equal.  The tokens decoded at the step (their scores lie
-  far below the threshold) are always selected.
+  rounding alone causes (oracle.storage_emulation over the always-computed
+  blocks) among the 2N tokens whose scores lie nearest the threshold (the
+  ones the ranking decides between; scores far from 1 move more, but only
+  the near-threshold ones can change places); on a slot whose threshold
+  gap exceeds 2 x band the sets must be equal.  The tokens decoded at the
+  step (their scores lie far below the threshold) are always selected.
 * outputs: the oracle runs the same steps with the GPU's selected rows as
   given rows (teacher forcing) and the GPU's outputs are bounded by the
   rule of the full-size tests, with the storage-rounding figures computed
@@ -102,7 +104,8 @@ def test_selection_valid_on_schedule_inputs():
             assert np.all(np.diff(got) > 0) and got.min() >= 0 and got.max() < d.seq_len
             order = np.sort(s)
             thr, gap = order[n - 1], order[n] - order[n - 1]
-            band = BAND_FACTOR * float(np.abs(s_emu - s).max())
+            near = np.argsort(np.abs(s - thr), kind="stable")[:2 * n]
+            band = BAND_FACTOR * float(np.abs(s_emu - s)[near].max())
             chosen = np.zeros(d.seq_len, dtype=bool)
             chosen[got] = True
             over = float((s[chosen] - thr).max())
