@@ -83,9 +83,12 @@ def _teacher_forced(hd, W, zc, zu, xi, scale, traj, eps, rows=None):
     print(f"  worst eps deviation {worst:.3f} of the bar; worst latent step deviation {worst_x:.2e}", flush=True)
 
 
+@pytest.mark.parametrize("width,cond", [(192, 128), (256, 512)])
 @pytest.mark.parametrize("scale", [1.0, 4.0])
-def test_head_small_ragged_rows(scale):
-    hd = HeadDims(width=192, depth=2, cond_dim=128, token_dim=16, steps=12, train_steps=120, freq_dim=64,
+def test_head_small_ragged_rows(scale, width, cond):
+    """Two widths, 37 tokens = 74 rows that end mid-tile, one token
+    conditioned on an index past the rows (read as a zero row)."""
+    hd = HeadDims(width=width, depth=2, cond_dim=cond, token_dim=16, steps=12, train_steps=120, freq_dim=64,
                   max_rows=64)
     W, zc, zu, x0, xi, x_out, traj, eps = _run(hd, 37, 90, scale, bad_index=True)
     np.testing.assert_array_equal(traj[0], x0)
