@@ -51,6 +51,11 @@ KIND_ROOFLINE = {
 }
 
 
+# how the metric names each workload (the headline is MAR-L, 64 images x 2 pathways)
+WORKLOAD_LABEL = {"mar-l": "MAR-L, 64x2 CFG", "mar-b": "MAR-B, 32x2 CFG", "mar-h": "MAR-H, 128x2 CFG",
+                  "mar-l-hires": "MAR-L at 1088 tokens, 32x2 CFG"}
+
+
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -544,7 +549,7 @@ def main():
         "tflops": tflops, "gbs": gbs,
     }
     line = {
-        "metric": f"cached MAR step tokens/s (MAR-L, 64x2 CFG, {n_steps}-step LazyMAR schedule)",
+        "metric": f"cached MAR step tokens/s ({WORKLOAD_LABEL[args.workload]}, {n_steps}-step LazyMAR schedule)",
         "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms_per_sched, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": dims.dtype, "data": "synthetic",
