@@ -18,8 +18,8 @@ Other options: --workload (the MAR-B, MAR-H and 1088-token shapes), --rule
 (the selection strategies of the paper's comparison), --score-source and
 --fresh-kv (the method's variants), --profile-kind (which kernel class the
 roofline reports, against the MFMA or the HBM peak).  --gemm-shapes,
---attention-shapes, --memory-shapes and --calibrate-copy only run single
-launches for hardware-counter passes.
+--attention-shapes, --memory-shapes, --head-shapes and --calibrate-copy only
+run single launches (or one head call) for trace and hardware-counter passes.
 
 Prints one JSON line.  --gpus N with N > 1 exits: the measurement is one GPU's share of the work.
 """
@@ -88,6 +88,9 @@ def parse():
     ap.add_argument("--memory-shapes", action="store_true",
                     help="only run the memory-bound kernels (LayerNorm dense and gather, scores, select) once "
                          "each at the MAR-L schedule's shapes (for hardware-counter runs)")
+    ap.add_argument("--head-shapes", action="store_true",
+                    help="only run one call of the MAR-L diffusion head on 256 tokens (for trace and "
+                         "hardware-counter runs)")
     ap.add_argument("--no-head", action="store_true",
                     help="skip the diffusion-head leg (the per-token head run for the tokens each decoding "
                          "step decodes, timed beside the transformer schedule)")
@@ -197,6 +200,36 @@ def attention_shapes():
     shapes = {f"{seqs}x{per}": c for (seqs, per), c in sorted(counts.items(), key=lambda kv: -kv[0][0] * kv[0][1])}
     print(json.dumps({"attention_shapes_to_launches_per_schedule": shapes, "heads": H, "seq": S, "d_head": dh}),
           flush=True)
+
+
+def head_shapes(tokens: int = 256):
+    """One call of the MAR-L diffusion head on `tokens` tokens (the 64-step schedule decodes
+    16384 tokens, 256 per step on average): 100 DDPM steps of both guidance branches, for
+    trace and hardware-counter runs.  Inputs are random rows of a transformer output."""
+    import torch
+
+    from paper_2503_12450_amd import binding as B
+    from paper_2503_12450_amd.device import upload_head
+    from paper_2503_12450_amd.flops import head_flops_per_eval
+    from paper_2503_12450_amd.workload import HEADS, head_weights
+
+    dev = "cuda:0"
+    hd = HEADS["mar-l"]
+    from dataclasses import replace
+    hd = replace(hd, max_rows=tokens)
+    head = B.MarHead(hd, upload_head(head_weights(hd), hd.dtype, device=dev))
+    g = torch.Generator(device=dev).manual_seed(0)
+    y = torch.randn(tokens, hd.cond_dim, device=dev, generator=g)
+    yu = torch.randn(tokens, hd.cond_dim, device=dev, generator=g)
+    rows = torch.arange(tokens, device=dev, dtype=torch.int32)
+    x0 = torch.randn(tokens, hd.token_dim, device=dev, generator=g)
+    xi = torch.randn(hd.steps, tokens, hd.token_dim, device=dev, generator=g)
+    xo = torch.empty(tokens, hd.token_dim, device=dev)
+    head.sample(y, yu, rows, rows, x0, xi, 4.0, xo)
+    torch.cuda.synchronize()
+    flops = head_flops_per_eval(hd) * 2 * tokens * hd.steps
+    print(json.dumps({"head": "mar-l", "width": hd.width, "depth": hd.depth, "tokens": tokens,
+                      "ddpm_steps": hd.steps, "flops_per_call": flops}), flush=True)
 
 
 def memory_shapes():
@@ -434,6 +467,9 @@ def main():
         return
     if args.memory_shapes:
         memory_shapes()
+        return
+    if args.head_shapes:
+        head_shapes()
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
