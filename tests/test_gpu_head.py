@@ -124,3 +124,32 @@ def test_head_rows_are_independent():
                 xi[:, 5:15].contiguous(), 3.0, part)
     torch.cuda.synchronize()
     assert torch.equal(part, full[5:15])
+
+
+@pytest.mark.parametrize("model", ["mar-b", "mar-h"])
+def test_head_other_model_widths(model):
+    """The MAR-B (width 1024, 6 blocks) and MAR-H (width 1536, 12 blocks)
+    heads, whose row kernels have their own width-specialised forms, on 9
+    tokens over 10 sampling steps of the respaced 1000-step schedule."""
+    hd = replace(HEADS[model], steps=10, max_rows=16)
+    W, zc, zu, x0, xi, x_out, traj, eps = _run(hd, 9, 40, 4.0, seed=7)
+    np.testing.assert_array_equal(traj[-1], x_out)
+    _teacher_forced(hd, W, zc, zu, xi, 4.0, traj, eps)
+
+
+def test_head_one_token_and_no_tokens():
+    """One token samples like any other (teacher-forced); zero tokens is a
+    no-op that leaves the output untouched."""
+    hd = HeadDims(width=128, depth=2, cond_dim=64, token_dim=16, steps=8, train_steps=80, freq_dim=64,
+                  max_rows=4)
+    W, zc, zu, x0, xi, x_out, traj, eps = _run(hd, 1, 3, 2.0, seed=9)
+    _teacher_forced(hd, W, zc, zu, xi, 2.0, traj, eps)
+    head = B.MarHead(hd, upload_head(W, hd.dtype))
+    y = to_device(normal_rows((3, hd.cond_dim), seed=31), "f32")
+    none = torch.empty(0, dtype=torch.int32, device=DEV)
+    x0e = torch.empty((0, hd.token_dim), device=DEV)
+    xie = torch.empty((hd.steps, 0, hd.token_dim), device=DEV)
+    out = torch.full((1, hd.token_dim), 7.0, device=DEV)
+    head.sample(y, y, none, none, x0e, xie, 2.0, out)
+    torch.cuda.synchronize()
+    assert torch.all(out == 7.0)
