@@ -19,7 +19,8 @@ Other options: --workload (the MAR-B, MAR-H and 1088-token shapes), --rule
 --fresh-kv (the method's variants), --profile-kind (which kernel class the
 roofline reports, against the MFMA or the HBM peak).  --gemm-shapes,
 --attention-shapes, --memory-shapes, --head-shapes and --calibrate-copy only
-run single launches (or one head call) for trace and hardware-counter passes.
+run single launches (or one head call) for trace and hardware-counter passes;
+--library-gemms times the products against the vendor library's.
 
 Prints one JSON line.  --gpus N with N > 1 exits: the measurement is one GPU's share of the work.
 """
@@ -91,6 +92,9 @@ def parse():
     ap.add_argument("--head-shapes", action="store_true",
                     help="only run one call of the MAR-L diffusion head on 256 tokens (for trace and "
                          "hardware-counter runs)")
+    ap.add_argument("--library-gemms", action="store_true",
+                    help="only time the block products (bias epilogue) against the vendor library's "
+                         "product of the same shape")
     ap.add_argument("--no-head", action="store_true",
                     help="skip the diffusion-head leg (the per-token head run for the tokens each decoding "
                          "step decodes, timed beside the transformer schedule)")
@@ -230,6 +234,49 @@ def head_shapes(tokens: int = 256):
     flops = head_flops_per_eval(hd) * 2 * tokens * hd.steps
     print(json.dumps({"head": "mar-l", "width": hd.width, "depth": hd.depth, "tokens": tokens,
                       "ddpm_steps": hd.steps, "flops_per_call": flops}), flush=True)
+
+
+def library_gemms():
+    """The block products with the bias epilogue against the vendor library's product of the
+    same shape (torch.nn.functional.linear, which dispatches to hipBLASLt), alternating, on the
+    dense (40960 rows) and cached (3200 rows) MAR-L shapes.  A reference point only: the path's
+    products carry fused epilogues the library call does not."""
+    import torch
+
+    from paper_2503_12450_amd import binding as B
+
+    dev = "cuda:0"
+    g = torch.Generator(device=dev).manual_seed(0)
+
+    def timed(fn, reps=10):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3
+
+    for name, M, N, K in (("qkv", 40960, 3072, 1024), ("proj", 40960, 1024, 1024), ("fc1", 40960, 4096, 1024),
+                          ("fc2", 40960, 1024, 4096), ("qkv", 3200, 3072, 1024), ("proj", 3200, 1024, 1024),
+                          ("fc1", 3200, 4096, 1024), ("fc2", 3200, 1024, 4096)):
+        a = torch.randn(M, K, device=dev, generator=g).to(torch.bfloat16)
+        w = (torch.randn(N, K, device=dev, generator=g) * 0.02).to(torch.bfloat16)
+        b32 = torch.randn(N, device=dev, generator=g) * 0.1
+        b16 = b32.to(torch.bfloat16)
+        out = torch.empty(M, N, device=dev, dtype=torch.bfloat16)
+        lib, ours = [], []
+        for _ in range(2):
+            lib.append(timed(lambda: torch.nn.functional.linear(a, w, b16)))
+            ours.append(timed(lambda: B.k_linear("bf16", a, w, b32, out, gelu=False)))
+        fl = 2.0 * M * N * K
+        print(json.dumps({"product": name, "m": M, "n": N, "k": K, "library_us": round(min(lib), 1),
+                          "path_us": round(min(ours), 1), "library_over_path_time": round(min(lib) / min(ours), 3),
+                          "library_tflops": round(fl / min(lib) / 1e6), "path_tflops": round(fl / min(ours) / 1e6)}),
+              flush=True)
 
 
 def memory_shapes():
@@ -470,6 +517,9 @@ def main():
         return
     if args.head_shapes:
         head_shapes()
+        return
+    if args.library_gemms:
+        library_gemms()
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
